@@ -1,0 +1,254 @@
+"""TEST INFRASTRUCTURE ONLY: the CPU oracle of one SkewAdam step.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py``
+may import this package. It shares no code with the GPU library: the step itself
+is plain C in ``skew_oracle.c`` (loaded through ctypes), and the closed-form state
+model of Eq. 2 / Table 6 is plain Python below.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass, field
+from typing import Iterable, Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libskew_oracle.so")
+SRC_PATH = os.path.join(HERE, "skew_oracle.c")
+
+BACKBONE, EXPERT, ROUTER = 0, 1, 2
+TIER_NAMES = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
+
+# Paper defaults (Alg. 1 caption, Table 5): beta = (0.9, 0.999), eps = 1e-8,
+# lr = 3e-4; update clipping at RMS 1 (Sec. 3).
+DEFAULTS = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the oracle with plain IEEE float semantics (no contraction, no fast-math)."""
+    cmd = ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared",
+           "-std=c11", "-Wall", "-o", LIB_PATH + ".tmp", SRC_PATH, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd, cwd=HERE)
+    os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+class _Tensor(ctypes.Structure):
+    _fields_ = [
+        ("tier", ctypes.c_int32), ("ndim", ctypes.c_int32),
+        ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+        ("tensor_id", ctypes.c_uint64),
+        ("w", ctypes.c_void_p), ("g", ctypes.c_void_p),
+        ("m", ctypes.c_void_p), ("v", ctypes.c_void_p),
+        ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
+        ("u_out", ctypes.c_void_p), ("x_out", ctypes.c_void_p), ("y_out", ctypes.c_void_p),
+        ("rms_out", ctypes.c_void_p),
+    ]
+
+
+class _HParams(ctypes.Structure):
+    _fields_ = [
+        ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+        ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float),
+        ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
+    ]
+
+
+_LIB = None
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        L.skew_oracle_step.argtypes = [ctypes.POINTER(_HParams), ctypes.POINTER(_Tensor), ctypes.c_int]
+        L.skew_oracle_step.restype = ctypes.c_int
+        L.skew_oracle_f32_to_bf16.argtypes = [ctypes.c_float]
+        L.skew_oracle_f32_to_bf16.restype = ctypes.c_uint16
+        L.skew_oracle_f32_to_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+        L.skew_oracle_mix64.argtypes = [ctypes.c_uint64]
+        L.skew_oracle_mix64.restype = ctypes.c_uint64
+        L.skew_oracle_fmix32.argtypes = [ctypes.c_uint32]
+        L.skew_oracle_fmix32.restype = ctypes.c_uint32
+        L.skew_oracle_key.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_uint64]
+        L.skew_oracle_key.restype = ctypes.c_uint64
+        L.skew_oracle_u16.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.skew_oracle_u16.restype = ctypes.c_uint32
+        L.skew_oracle_u16_array.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
+        L.skew_oracle_threads.restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+@dataclass
+class Tensor:
+    """One parameter tensor and its state, as dense row-major numpy arrays."""
+    tier: int
+    w: np.ndarray                 # uint16 bf16 bits, shape (rows, cols) or (n,)
+    g: np.ndarray                 # uint16 bf16 bits, same shape
+    tensor_id: int
+    m: Optional[np.ndarray] = None
+    v: Optional[np.ndarray] = None
+    r: Optional[np.ndarray] = None
+    c: Optional[np.ndarray] = None
+    u_out: Optional[np.ndarray] = field(default=None, repr=False)
+    x_out: Optional[np.ndarray] = field(default=None, repr=False)
+    y_out: Optional[np.ndarray] = field(default=None, repr=False)
+    rms: float = float("nan")
+
+    @property
+    def ndim(self) -> int:
+        return self.w.ndim
+
+    @property
+    def rows_cols(self):
+        if self.w.ndim == 1:
+            return 1, int(self.w.shape[0])
+        return int(self.w.shape[0]), int(self.w.shape[1])
+
+    def init_state(self):
+        """Allocate zeroed state for this tensor's tier (Fig. 1, Table 6)."""
+        n, m = self.rows_cols
+        shape = self.w.shape
+        exact = self.tier == ROUTER or self.ndim == 1
+        if self.tier == BACKBONE:
+            self.m = np.zeros(shape, np.float32)
+        if exact:
+            self.v = np.zeros(shape, np.float32)
+        else:
+            self.r = np.zeros(n, np.float32)
+            self.c = np.zeros(m, np.float32)
+        return self
+
+
+def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAULTS["lr"],
+         beta1: float = DEFAULTS["beta1"], beta2: float = DEFAULTS["beta2"], eps: float = DEFAULTS["eps"],
+         clip_threshold: float = DEFAULTS["clip_threshold"], want_u: bool = False, want_x: bool = False,
+         want_y: bool = False) -> int:
+    """Run one oracle step over ``tensors`` in place. Returns the C status."""
+    tensors = list(tensors)
+    arr = (_Tensor * max(1, len(tensors)))()
+    rms = np.full(max(1, len(tensors)), np.nan, np.float64)
+    keep = []
+    for k, t in enumerate(tensors):
+        for name in ("w", "g", "m", "v", "r", "c"):
+            a = getattr(t, name)
+            if a is not None:
+                assert a.flags["C_CONTIGUOUS"], name
+        assert t.w.dtype == np.uint16 and t.g.dtype == np.uint16 and t.w.shape == t.g.shape
+        n, m = t.rows_cols
+        exact = t.tier == ROUTER or t.ndim == 1
+        if n * m > 0:
+            if t.tier == BACKBONE:
+                assert t.m is not None and t.m.dtype == np.float32 and t.m.size == n * m
+            if exact:
+                assert t.v is not None and t.v.dtype == np.float32 and t.v.size == n * m
+            else:
+                assert t.r is not None and t.r.size == n and t.c is not None and t.c.size == m
+        if want_u:
+            t.u_out = np.empty(t.w.shape, np.float32)
+        if want_x:
+            t.x_out = np.empty(t.w.shape, np.float32)
+        if want_y:
+            t.y_out = np.empty(t.w.shape, np.float32)
+        arr[k] = _Tensor(t.tier, t.ndim, n, m, t.tensor_id, _ptr(t.w), _ptr(t.g), _ptr(t.m), _ptr(t.v),
+                         _ptr(t.r), _ptr(t.c), _ptr(t.u_out), _ptr(t.x_out), _ptr(t.y_out),
+                         rms.ctypes.data + 8 * k)
+        keep.append(t)
+    hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1))
+    rc = lib().skew_oracle_step(ctypes.byref(hp), arr, len(tensors))
+    for k, t in enumerate(tensors):
+        t.rms = float(rms[k])
+    return rc
+
+
+def bf16_rne(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bits, round to nearest even (the cast of Alg. 1)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint16)
+    lib().skew_oracle_f32_to_bf16_array(x.ctypes.data, out.ctypes.data, x.size)
+    return out
+
+
+def bf16_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def mix64(z: int) -> int:
+    return int(lib().skew_oracle_mix64(z & (2**64 - 1)))
+
+
+def fmix32(h: int) -> int:
+    return int(lib().skew_oracle_fmix32(h & 0xFFFFFFFF))
+
+
+def dither_key(seed: int, step: int, tensor_id: int) -> int:
+    return int(lib().skew_oracle_key(seed & (2**64 - 1), step, tensor_id & (2**64 - 1)))
+
+
+def dither_u16(key: int, idx0: int, n: int) -> np.ndarray:
+    out = np.empty(n, np.uint32)
+    lib().skew_oracle_u16_array(key, idx0, n, out.ctypes.data)
+    return out
+
+
+def threads() -> int:
+    return int(lib().skew_oracle_threads())
+
+
+# ----------------------------------------------------------------------------------------
+# Closed-form state model: Eq. 2 plus the exact-v term of the vector parameters (Table 6).
+# ----------------------------------------------------------------------------------------
+POLICIES = ("skewadam", "expert_momentum", "factored_router", "uniform")
+
+
+def tensor_state_parts(tier: int, shape, policy: str = "skewadam") -> dict:
+    """fp32 state entries one tensor keeps under a tier policy, split by kind.
+
+    ``m``: momentum; ``v``: exact second moment; ``rc``: factored row + column
+    statistics (Fig. 1; Sec. 3 "The tiers"; Table 3 for the variant policies).
+    """
+    assert policy in POLICIES
+    dims = tuple(int(s) for s in shape)
+    N = int(np.prod(dims, dtype=np.int64)) if dims else 1
+    parts = {"m": 0, "v": 0, "rc": 0}
+    if N == 0:
+        return parts
+    momentum = tier == BACKBONE or (tier == EXPERT and policy in ("expert_momentum", "uniform")) \
+        or (tier == ROUTER and policy == "uniform")
+    if len(dims) == 1:
+        parts["v"] = N                     # vectors keep an exact v (Alg. 1)
+    elif tier == ROUTER and policy not in ("factored_router", "uniform"):
+        parts["v"] = N                     # the router keeps an exact v (Sec. 3, "The tiers")
+    else:
+        n, m = dims[-2], dims[-1]
+        lead = N // (n * m)                # stacked (E, n, m) tensors factor over the last two axes
+        parts["rc"] = lead * (n + m)       # Eq. 1: R in R^n, C in R^m
+    if momentum:
+        parts["m"] = N
+    return parts
+
+
+def tensor_state_floats(tier: int, shape, policy: str = "skewadam") -> int:
+    return sum(tensor_state_parts(tier, shape, policy).values())
+
+
+def state_bytes(tensors, policy: str = "skewadam") -> int:
+    """Eq. 2 (plus vector v): 4 bytes per fp32 state entry; ``tensors`` = iterable of (tier, shape)."""
+    return 4 * sum(tensor_state_floats(t, s, policy) for t, s in tensors)
+
+
+def adamw_state_bytes(tensors) -> int:
+    """AdamW keeps two fp32 moments per parameter (8 bytes, Sec. 1)."""
+    return 8 * sum(int(np.prod(s, dtype=np.int64)) for _, s in tensors)

@@ -1,0 +1,242 @@
+/*
+ * skew_oracle.c -- TEST INFRASTRUCTURE ONLY (see skew_oracle.h).
+ *
+ * One SkewAdam step, written out in the order of Alg. 1 with plain loops.
+ * Build: -O2 -ffp-contract=off -fno-fast-math, so that every float operation
+ * below is one IEEE-754 binary32 operation and the only fused multiply-adds
+ * are the explicit fmaf() calls. OpenMP splits independent rows (or column
+ * ranges); every sum keeps its ascending index order, so the result does not
+ * depend on the thread count.
+ *
+ * Step definition (all scalars float32 unless noted; N = rows*cols; idx = i*cols + j):
+ *   host scalars, in double then rounded once:  a1 = 1-b1, a2 = 1-b2,
+ *       s_m = sqrt(1-b2^t)/(1-b1^t)  (backbone bias correction, Alg. 1),
+ *       s_0 = sqrt(1-b2^t)           (momentum-free tiers, Alg. 1)
+ *   factored tensors (matrix, tier != router), Eq. 1 and the rank-one
+ *   reconstruction that follows it:
+ *       r_i = mean_j g_ij^2, c_j = mean_i g_ij^2   (double, rounded once)
+ *       R_i <- fmaf(a2, r_i, b2*R_i);  C_j <- fmaf(a2, c_j, b2*C_j)
+ *       Rbar = mean_i R_i (double, rounded once);  c'_j = C_j / max(Rbar, eps)
+ *       D_ij = sqrt(max(R_i * c'_j, eps))
+ *   exact tensors (router tier, or any vector), Alg. 1:
+ *       V <- fmaf(a2, g*g, b2*V);  D = sqrt(max(V, eps))
+ *   backbone: M <- fmaf(a1, g, b1*M);  Uhat = (s_m*M) / D
+ *   others:   Uhat = (s_0*g) / D
+ *   clip (Sec. 3, Alg. 1): k = 1 / max(1, RMS(Uhat)/d) with RMS over all N
+ *       (sum of squares in double);  U = Uhat*k
+ *   write-back (Sec. 3, Alg. 1): x = fmaf(-lr, U, w)
+ *       xi = e * 2^-24 * |w|, e = 2*u16 + 1 - 2^16  (uniform on +-ulp(w)/2 with
+ *       ulp(w) taken as 2^-7|w|, on a 2^-16 grid), added with one rounding:
+ *       y = fmaf(e*2^-24, |w|, x);  W' = bf16 round-to-nearest-even(y)
+ *   max() here propagates NaN (as torch.clamp does), so non-finite gradients
+ *   reach the weights instead of being floored away.
+ */
+#include "skew_oracle.h"
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define COL_BLOCK 256
+
+typedef struct {
+  float b1, a1, b2, a2, eps, d, lr, s_m, s_0;
+  int64_t step;
+  uint64_t seed;
+} consts_t;
+
+static float bf16_bits_to_f32(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return f;
+}
+
+/* round-to-nearest, ties-to-even, from float32 to the upper 16 bits; NaN -> 0x7FC0 */
+uint16_t skew_oracle_f32_to_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  if (f != f) return 0x7FC0;
+  uint32_t keep = u >> 16, drop = u & 0xFFFFu;
+  if (drop > 0x8000u || (drop == 0x8000u && (keep & 1u))) keep += 1u;
+  return (uint16_t)keep;
+}
+
+void skew_oracle_f32_to_bf16_array(const float *x, uint16_t *out, int64_t n) {
+  for (int64_t i = 0; i < n; i++) out[i] = skew_oracle_f32_to_bf16(x[i]);
+}
+
+/* SplitMix64 output mixing function (Steele, Lea and Flood, OOPSLA 2014). */
+static uint64_t splitmix64_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* MurmurHash3 32-bit finalizer (Appleby, public domain). */
+static uint32_t murmur3_fmix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  h *= 0xC2B2AE35u;
+  h ^= h >> 16;
+  return h;
+}
+
+uint64_t skew_oracle_mix64(uint64_t z) { return splitmix64_mix(z); }
+uint32_t skew_oracle_fmix32(uint32_t h) { return murmur3_fmix32(h); }
+
+/* per-(seed, step, tensor) dither key */
+uint64_t skew_oracle_key(uint64_t seed, int64_t step, uint64_t tensor_id) {
+  uint64_t k = splitmix64_mix(seed);
+  k = splitmix64_mix(k ^ (uint64_t)step);
+  return splitmix64_mix(k ^ tensor_id);
+}
+
+/* 16 uniform bits for element idx: one 32-bit hash per element pair (idx>>1);
+ * the even element takes the low half, the odd element the high half. */
+uint32_t skew_oracle_u16(uint64_t key, uint64_t idx) {
+  uint64_t pair = idx >> 1;
+  uint32_t hi = murmur3_fmix32((uint32_t)(pair >> 32) ^ (uint32_t)(key >> 32));
+  uint32_t h = murmur3_fmix32((uint32_t)pair ^ (uint32_t)key ^ hi);
+  return (idx & 1u) ? (h >> 16) : (h & 0xFFFFu);
+}
+
+void skew_oracle_u16_array(uint64_t key, uint64_t idx0, int64_t n, uint32_t *out) {
+  for (int64_t i = 0; i < n; i++) out[i] = skew_oracle_u16(key, idx0 + (uint64_t)i);
+}
+
+int skew_oracle_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+static float max_nan(float a, float b) { return (a != a) ? a : (a < b ? b : a); }
+
+static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
+  const int64_t n = T->rows, m = T->cols, N = n * m;
+  if (n <= 0 || m <= 0) return;
+  const int exact = (T->tier == ORACLE_ROUTER) || (T->ndim == 1);
+  const int momentum = (T->tier == ORACLE_BACKBONE);
+  float *uhat = (float *)malloc((size_t)N * sizeof(float));
+  double *row_ss = (double *)malloc((size_t)n * sizeof(double));
+  float *cprime = NULL;
+
+  if (!exact) {
+    /* Eq. 1, rows: mean over columns of G*G, then the EMA of R. */
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+      double s = 0.0;
+      for (int64_t j = 0; j < m; j++) {
+        double gv = bf16_bits_to_f32(T->g[i * m + j]);
+        s += gv * gv;
+      }
+      float ri = (float)(s / (double)m);
+      T->r[i] = fmaf(K->a2, ri, K->b2 * T->r[i]);
+    }
+    /* Eq. 1, columns: mean over rows of G*G (each column summed in row order). */
+    double *cs = (double *)calloc((size_t)m, sizeof(double));
+#pragma omp parallel for schedule(static)
+    for (int64_t jb = 0; jb < m; jb += COL_BLOCK) {
+      int64_t je = jb + COL_BLOCK < m ? jb + COL_BLOCK : m;
+      for (int64_t i = 0; i < n; i++)
+        for (int64_t j = jb; j < je; j++) {
+          double gv = bf16_bits_to_f32(T->g[i * m + j]);
+          cs[j] += gv * gv;
+        }
+    }
+    for (int64_t j = 0; j < m; j++) {
+      float cj = (float)(cs[j] / (double)n);
+      T->c[j] = fmaf(K->a2, cj, K->b2 * T->c[j]);
+    }
+    free(cs);
+    /* rank-one reconstruction V = R C^T / mean(R), with the mean clamped at eps */
+    double sr = 0.0;
+    for (int64_t i = 0; i < n; i++) sr += (double)T->r[i];
+    float rbar = (float)(sr / (double)n);
+    float q = max_nan(rbar, K->eps);
+    cprime = (float *)malloc((size_t)m * sizeof(float));
+    for (int64_t j = 0; j < m; j++) cprime[j] = T->c[j] / q;
+  }
+
+  /* preconditioned update and its sum of squares, row by row */
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; i++) {
+    double s = 0.0;
+    for (int64_t j = 0; j < m; j++) {
+      const int64_t idx = i * m + j;
+      const float g = bf16_bits_to_f32(T->g[idx]);
+      float dd;
+      if (exact) {
+        T->v[idx] = fmaf(K->a2, g * g, K->b2 * T->v[idx]);
+        dd = sqrtf(max_nan(T->v[idx], K->eps));
+      } else {
+        float vhat = T->r[i] * cprime[j];
+        dd = sqrtf(max_nan(vhat, K->eps));
+      }
+      float num;
+      if (momentum) {
+        T->m[idx] = fmaf(K->a1, g, K->b1 * T->m[idx]);
+        num = K->s_m * T->m[idx];
+      } else {
+        num = K->s_0 * g;
+      }
+      const float u = num / dd;
+      uhat[idx] = u;
+      s += (double)u * (double)u;
+    }
+    row_ss[i] = s;
+  }
+  double ss = 0.0;
+  for (int64_t i = 0; i < n; i++) ss += row_ss[i];
+
+  /* update clipping to RMS d */
+  const double rms = sqrt(ss / (double)N);
+  if (T->rms_out) *T->rms_out = rms;
+  const double ratio = rms / (double)K->d;
+  const double den = (ratio != ratio) ? ratio : (ratio < 1.0 ? 1.0 : ratio);
+  const float kclip = (float)(1.0 / den);
+
+  /* dithered bf16 write-back */
+  const uint64_t key = skew_oracle_key(K->seed, K->step, T->tensor_id);
+#pragma omp parallel for schedule(static)
+  for (int64_t idx = 0; idx < N; idx++) {
+    const float w = bf16_bits_to_f32(T->w[idx]);
+    const float U = uhat[idx] * kclip;
+    const float x = fmaf(-K->lr, U, w);
+    const int32_t e = 2 * (int32_t)skew_oracle_u16(key, (uint64_t)idx) + 1 - 65536;
+    const float f = (float)e * 0x1p-24f;
+    const float y = fmaf(f, fabsf(w), x);
+    if (T->u_out) T->u_out[idx] = U;
+    if (T->x_out) T->x_out[idx] = x;
+    if (T->y_out) T->y_out[idx] = y;
+    T->w[idx] = skew_oracle_f32_to_bf16(y);
+  }
+  free(cprime);
+  free(row_ss);
+  free(uhat);
+}
+
+int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n) {
+  if (hp->step < 1) return -1;
+  consts_t K;
+  const double b1 = hp->beta1, b2 = hp->beta2, tt = (double)hp->step;
+  K.b1 = hp->beta1;
+  K.a1 = (float)(1.0 - b1);
+  K.b2 = hp->beta2;
+  K.a2 = (float)(1.0 - b2);
+  K.eps = hp->eps;
+  K.d = hp->clip_threshold;
+  K.lr = hp->lr;
+  K.s_m = (float)(sqrt(1.0 - pow(b2, tt)) / (1.0 - pow(b1, tt)));
+  K.s_0 = (float)sqrt(1.0 - pow(b2, tt));
+  K.step = hp->step;
+  K.seed = hp->seed;
+  for (int i = 0; i < n; i++) step_tensor(&K, &t[i]);
+  return 0;
+}

@@ -1,0 +1,62 @@
+/*
+ * skew_oracle.h -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-source CPU oracle of one SkewAdam optimizer step
+ * (Sec. 3 "SkewAdam: tiered state allocation", Eq. 1, Alg. 1). It exists to
+ * check the GPU library; only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load it. It shares no code, header or
+ * constant with the GPU library.
+ *
+ * Arithmetic: float32 as the paper's step is "computed in float32" (Sec. 3,
+ * "Update clipping and low-precision updates"); every reduction is carried in
+ * double in ascending index order and rounded to float once.
+ */
+#ifndef SKEW_ORACLE_H
+#define SKEW_ORACLE_H
+#include <stdint.h>
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORACLE_BACKBONE = 0, ORACLE_EXPERT = 1, ORACLE_ROUTER = 2 };
+
+typedef struct {
+  int32_t tier;       /* ORACLE_BACKBONE / ORACLE_EXPERT / ORACLE_ROUTER */
+  int32_t ndim;       /* 1 = vector, 2 = matrix */
+  int64_t rows, cols; /* dense row-major, rows*cols elements */
+  uint64_t tensor_id; /* keys the dither */
+  uint16_t *w;        /* bf16 bits, updated in place */
+  const uint16_t *g;  /* bf16 bits */
+  float *m;           /* momentum [rows*cols] (backbone) or NULL */
+  float *v;           /* exact second moment [rows*cols] (router, vectors) or NULL */
+  float *r;           /* factored row statistic [rows] or NULL */
+  float *c;           /* factored column statistic [cols] or NULL */
+  float *u_out;       /* optional [rows*cols]: the clipped update U */
+  float *x_out;       /* optional [rows*cols]: W - lr*U before the dither */
+  float *y_out;       /* optional [rows*cols]: the float value handed to the bf16 cast */
+  double *rms_out;    /* optional: RMS of the unclipped update of this tensor */
+} skew_oracle_tensor;
+
+typedef struct {
+  float lr, beta1, beta2, eps, clip_threshold;
+  int64_t step;  /* t >= 1 */
+  uint64_t seed;
+} skew_oracle_hparams;
+
+/* One step over n tensors. Returns 0, or -1 when step < 1. */
+int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n);
+
+/* Pieces exposed for pinning. */
+uint16_t skew_oracle_f32_to_bf16(float f);
+void skew_oracle_f32_to_bf16_array(const float *x, uint16_t *out, int64_t n);
+uint64_t skew_oracle_mix64(uint64_t z);
+uint32_t skew_oracle_fmix32(uint32_t h);
+uint64_t skew_oracle_key(uint64_t seed, int64_t step, uint64_t tensor_id);
+uint32_t skew_oracle_u16(uint64_t key, uint64_t idx);
+void skew_oracle_u16_array(uint64_t key, uint64_t idx0, int64_t n, uint32_t *out);
+int skew_oracle_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,109 @@
+"""Pins the oracle's float32 -> bf16 cast (round to nearest even, the cast of
+Alg. 1) to PyTorch's CPU conversion, and its two hash mixers to their published
+outputs; checks the dither hash's statistics (uniform, uncorrelated along
+elements, across steps and across tensors)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _torch_bf16_bits(x: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def test_rne_structured_sweep_matches_torch():
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0x0000, 0x0001, 0x3FFF, 0x7FFF, 0x8000, 0x8001, 0xBFFF, 0xFFFF], np.uint32)
+    bits = (hi[:, None] | lows[None, :]).ravel()
+    x = bits.view(np.float32)
+    mine = oracle.bf16_rne(x)
+    ref = _torch_bf16_bits(x)
+    nan = np.isnan(x)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    # NaN stays NaN (the payload is not part of the contract)
+    assert np.all((mine[nan] & 0x7F80) == 0x7F80) and np.all((mine[nan] & 0x007F) != 0)
+
+
+def test_rne_random_patterns_match_torch():
+    rng = np.random.default_rng(1234)
+    bits = rng.integers(0, 1 << 32, size=4_000_000, dtype=np.uint64).astype(np.uint32)
+    x = bits.view(np.float32)
+    keep = ~np.isnan(x)
+    assert np.array_equal(oracle.bf16_rne(x[keep]), _torch_bf16_bits(x[keep]))
+
+
+def test_rne_ties_go_to_even():
+    # 1 + 2^-8 lies halfway between bf16 1.0 and 1 + 2^-7: ties to the even (1.0)
+    assert oracle.bf16_rne(np.array([1.0 + 2.0**-8], np.float32))[0] == 0x3F80
+    # 1 + 3*2^-8 lies halfway between 1 + 2^-7 (odd) and 1 + 2^-6: goes up
+    assert oracle.bf16_rne(np.array([1.0 + 3 * 2.0**-8], np.float32))[0] == 0x3F82
+    # largest finite bf16 plus half an ulp rounds to infinity
+    assert oracle.bf16_rne(np.array([np.float32(3.3961775e38)], np.float32))[0] == 0x7F80
+
+
+def test_mixers_match_published_vectors():
+    n = 0
+    for line in open(os.path.join(GOLD, "hash_vectors.txt")):
+        line = line.split("|")[0].strip()
+        if not line or line.startswith("#"):
+            continue
+        fn, x, y = line.split()
+        f = oracle.mix64 if fn == "mix64" else oracle.fmix32
+        assert f(int(x, 16)) == int(y, 16), line
+        n += 1
+    assert n == 6
+
+
+def test_key_depends_on_every_input():
+    base = oracle.dither_key(0, 1, 7)
+    assert base == oracle.dither_key(0, 1, 7)
+    others = {oracle.dither_key(1, 1, 7), oracle.dither_key(0, 2, 7), oracle.dither_key(0, 1, 8)}
+    assert base not in others and len(others) == 3
+
+
+def test_u16_range_and_pairing():
+    key = oracle.dither_key(3, 5, 11)
+    u = oracle.dither_u16(key, 0, 1 << 12)
+    assert u.max() < 65536
+    # elements 2p and 2p+1 take the two halves of one 32-bit hash of p
+    h = np.array([oracle.fmix32((p ^ (key & 0xFFFFFFFF) ^ oracle.fmix32(key >> 32)) & 0xFFFFFFFF)
+                  for p in range(1 << 11)], np.uint64)
+    assert np.array_equal(u[0::2], (h & 0xFFFF).astype(np.uint32))
+    assert np.array_equal(u[1::2], (h >> 16).astype(np.uint32))
+
+
+def _chi2_p(counts):
+    from scipy.stats import chisquare
+    return chisquare(counts).pvalue
+
+
+def test_u16_uniform_and_uncorrelated():
+    n = 1 << 20
+    key = oracle.dither_key(0, 1, 0)
+    u = oracle.dither_u16(key, 0, n).astype(np.int64)
+    assert _chi2_p(np.bincount(u >> 8, minlength=256)) > 1e-4
+    assert _chi2_p(np.bincount(u & 0xFF, minlength=256)) > 1e-4
+    assert abs(u.mean() / 65535.0 - 0.5) < 5e-3
+    z = (u - 32767.5) / 18918.6
+    lim = 5.0 / np.sqrt(n)
+    assert abs(np.mean(z[1:] * z[:-1])) < lim            # along elements (within and across pairs)
+    assert abs(np.mean(z[2:] * z[:-2])) < lim
+    u2 = oracle.dither_u16(oracle.dither_key(0, 2, 0), 0, n).astype(np.int64)   # next step
+    assert abs(np.mean(z * (u2 - 32767.5) / 18918.6)) < lim
+    u3 = oracle.dither_u16(oracle.dither_key(0, 1, 1), 0, n).astype(np.int64)   # next tensor
+    assert abs(np.mean(z * (u3 - 32767.5) / 18918.6)) < lim
+
+
+def test_u16_high_element_indices():
+    # indices past 2^32 pairs mix the upper half of the pair index in
+    key = oracle.dither_key(0, 1, 0)
+    a = oracle.dither_u16(key, 0, 4096)
+    b = oracle.dither_u16(key, 1 << 33, 4096)
+    assert not np.array_equal(a, b)
+    assert abs(b.astype(np.float64).mean() / 65535 - 0.5) < 0.05

@@ -1,0 +1,151 @@
+/*
+ * skewadam.h -- C ABI of the SkewAdam optimizer step for AMD Instinct MI355X (gfx950).
+ *
+ * One call to skew_step() applies one SkewAdam step (Sec. 3 "SkewAdam: tiered
+ * state allocation", Eq. 1, Alg. 1) to every tensor of a descriptor table.
+ * Each tensor gets the state of its tier (Fig. 1; Sec. 3 "The tiers"):
+ *   BACKBONE matrix : fp32 momentum M [rows*cols] + factored second moment R [rows], C [cols]
+ *   BACKBONE vector : fp32 momentum M + exact second moment V [len]
+ *   EXPERT   matrix : factored second moment R, C only
+ *   EXPERT   vector : exact V
+ *   ROUTER   (any)  : exact V [rows*cols]
+ * Every tier then clips its update to RMS <= clip_threshold (Sec. 3 "Update
+ * clipping"; Alg. 1) and writes the weight back as bf16 through a dithered
+ * round-to-nearest-even cast (Sec. 3 "Update clipping and low-precision
+ * updates"; Alg. 1).
+ *
+ * Conventions
+ *  - Every function returns an int status: SKEW_OK (0) or a negative SKEW_E* code.
+ *    Nothing aborts or throws. A call that fails validation launches nothing.
+ *  - "device" pointers are HIP device allocations on the current device;
+ *    "host" pointers are ordinary host memory. The caller owns all of them.
+ *  - Streams are hipStream_t values passed as void* (NULL = the default stream).
+ *    skew_state_init and skew_step are stream-ordered and never synchronise the
+ *    device, except skew_state_init, which waits for its own table upload.
+ *  - bf16 is IEEE binary32 truncated to its upper 16 bits (the bfloat16 format).
+ *  - Sizes and element indices are 64-bit throughout (tensors of >= 2^31 elements).
+ */
+#ifndef SKEWADAM_H
+#define SKEWADAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SKEW_ABI_VERSION 1
+
+enum {
+  SKEW_OK = 0,
+  SKEW_EINVAL = -1,    /* bad argument: tier, ndim, shape, ld, NULL pointer, hyper-parameter */
+  SKEW_ENOSPACE = -2,  /* a caller buffer is smaller than skew_state_bytes() asked for */
+  SKEW_EHIP = -3,      /* the HIP runtime reported an error (launch, copy, memset) */
+  SKEW_ENOMEM = -4     /* host allocation of the context failed */
+};
+
+enum { SKEW_TIER_BACKBONE = 0, SKEW_TIER_EXPERT = 1, SKEW_TIER_ROUTER = 2 };
+
+/* One parameter tensor (Sec. 3 "The tiers": the policy assigns state by parameter role).
+ *   tier      SKEW_TIER_*.
+ *   ndim      2 = matrix (row-major, `rows` x `cols`, row stride `ld` elements);
+ *             1 = vector of rows*cols elements (one of rows, cols must be 1), contiguous.
+ *             Matrices outside the router tier take the factored second moment (Eq. 1);
+ *             the router and every vector take the exact one (Alg. 1).
+ *   rows, cols  >= 0. A tensor with no elements is accepted and skipped.
+ *   ld        row stride in elements, >= cols (ignored for vectors).
+ *   tensor_id caller-chosen, stable across runs and checkpoints; keys the dither, so
+ *             two tensors should not share an id.
+ *   w         device, bf16 [rows x ld], read and written in place by skew_step.
+ *   g         device, bf16 [rows x ld], read only.
+ *   m, v, r, c  OUT: filled by skew_state_init with pointers into the caller's state
+ *             buffer (NULL where the tier keeps no such state); dense, row-major:
+ *             m, v [rows*cols] (element (i, j) at i*cols + j), r [rows], c [cols].
+ * w and g may have any alignment; 16-byte-aligned rows (w, g aligned and ld a
+ * multiple of 8) take the vectorised path. */
+typedef struct skew_tensor_desc {
+  int32_t tier;
+  int32_t ndim;
+  int64_t rows;
+  int64_t cols;
+  int64_t ld;
+  uint64_t tensor_id;
+  void *w;
+  const void *g;
+  float *m;
+  float *v;
+  float *r;
+  float *c;
+} skew_tensor_desc;
+
+/* Hyper-parameters of one step (Alg. 1; defaults of Table 5: lr 3e-4,
+ * beta = (0.9, 0.999), eps 1e-8; clip threshold 1 from Sec. 3).
+ *   lr              eta_t, the caller's schedule value for this step (finite).
+ *   beta1, beta2    in [0, 1).
+ *   eps             > 0: floor of the second moment, and of mean(R) in the
+ *                   factored reconstruction.
+ *   clip_threshold  d > 0 (may be +inf: no clipping): U <- U / max(1, RMS(U)/d).
+ *   flags           must be 0.
+ *   step            t >= 1, the caller's step counter (the library keeps none).
+ *   seed            dither seed; with (step, tensor_id, element index) it fixes
+ *                   every dither value, so results are bit-reproducible. */
+typedef struct skew_hparams {
+  float lr;
+  float beta1;
+  float beta2;
+  float eps;
+  float clip_threshold;
+  int32_t flags;
+  int64_t step;
+  uint64_t seed;
+} skew_hparams;
+
+typedef struct skew_ctx skew_ctx;
+
+/* Sizes of the two caller-owned device buffers for a descriptor table (Eq. 2:
+ * S = 4[N_bb + sum(n_W + m_W) + N_rt] bytes, plus the exact v of vectors as in
+ * Table 6; each state slice is padded to 256 bytes).
+ *   d, n              host array of n >= 0 descriptors (only shape fields are read).
+ *   state_bytes       OUT: bytes of fp32 state (>= the closed form).
+ *   workspace_bytes   OUT: bytes of scratch the library needs (tables and partial sums).
+ * Host only; needs no GPU. Errors: SKEW_EINVAL. */
+int skew_state_bytes(const skew_tensor_desc *d, int n, size_t *state_bytes, size_t *workspace_bytes);
+
+/* Create a context for the table d[0..n).
+ *   ctx         OUT: the new context (host object) or NULL on error.
+ *   d           host array; its m, v, r, c fields are filled in (see above).
+ *   state       device buffer of >= skew_state_bytes() bytes; carved into the state
+ *               slices and zero-filled on `stream`. It holds every byte of optimizer
+ *               state: saving it with the step counter and seed is a checkpoint, and
+ *               copying it back after a new skew_state_init() on an identical table
+ *               resumes bit-exactly.
+ *   workspace   device buffer of >= workspace_bytes; the library owns its contents
+ *               until skew_destroy().
+ *   stream      hipStream_t as void*.
+ * All pointers must stay valid and unchanged until skew_destroy(); to change them,
+ * destroy and init again. Errors: SKEW_EINVAL, SKEW_ENOSPACE, SKEW_ENOMEM, SKEW_EHIP. */
+int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
+/* One SkewAdam step (Alg. 1) over every tensor of ctx, enqueued on `stream`
+ * (asynchronous; errors of the kernels themselves surface at the caller's next
+ * synchronisation). Reads g, updates w and the state in place. One step per
+ * context may be in flight at a time. Non-finite gradients propagate into the
+ * state and weights (a NaN makes the clip factor NaN, so its whole tensor).
+ * Errors: SKEW_EINVAL (ctx NULL, hp invalid), SKEW_EHIP (launch failed). */
+int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream);
+
+/* Free the host context. Does not touch device memory. NULL is a no-op. */
+void skew_destroy(skew_ctx *ctx);
+
+/* Static description of a status code (never NULL). */
+const char *skew_strerror(int status);
+
+/* SKEW_ABI_VERSION of the loaded library. */
+int skew_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SKEWADAM_H */

@@ -1,0 +1,88 @@
+// skew_internal.h -- structures shared by the planner, the C ABI and the kernels.
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/skewadam.h"
+
+namespace skew {
+
+enum Kind : int32_t { kFactored = 0, kExact = 1 };
+
+constexpr int kThreads = 256;           // threads per work-group (4 wave64)
+constexpr int kWaves = kThreads / 64;
+constexpr int kChunk = 512;             // columns one wave covers with one 16-byte load per lane
+constexpr int kMaxCw = 4;               // at most 4 chunks (2048 columns) per tile row
+constexpr int kFold = 256;              // rows (or columns) folded by one work-group
+constexpr int64_t kTileElems = 1 << 19; // target elements per tile: 1 MiB of bf16 gradient
+constexpr size_t kAlign = 256;
+
+// Device-resident description of one tensor, its state and its partial sums.
+struct DevTensor {
+  uint16_t *w;
+  const uint16_t *g;
+  float *M, *V, *R, *C;   // state (NULL where the tier keeps none)
+  double *rowpart;        // [ntc][n]   partial row sums of g^2, one per column strip
+  double *colpart;        // [ntr][m]   partial column sums of g^2, one per row band
+  double *ainv;           // [n]        1/sqrt(R_i) after the step's EMA
+  double *rsum;           // [nfr]      sums of R_i over each fold chunk of rows
+  double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
+  int64_t n, m, ld;       // rows, columns, row stride (elements)
+  int64_t tr;             // rows per tile
+  int32_t cw;             // 512-column chunks per tile (1..4)
+  int32_t ntc, ntr;       // column strips, row bands
+  int32_t nfr, nfc;       // fold work-groups over rows, over columns
+  int32_t kind;           // kFactored / kExact
+  int32_t momentum;       // backbone tier
+  int32_t vec;            // 16-byte aligned rows: vector loads and stores
+  uint64_t tensor_id;
+};
+
+struct Item {
+  int32_t tensor;
+  int32_t tile;
+};
+
+// Per-step scalars (Alg. 1), computed on the host in double and rounded once.
+struct StepConsts {
+  float b1, a1, b2, a2, eps, lr, d, s_m, s_0;
+  int32_t pad;
+  int64_t step;
+  uint64_t seed;
+};
+
+// Host-side plan of a descriptor table.
+struct TensorPlan {
+  int64_t n = 0, m = 0, ld = 0, N = 0;
+  int32_t tier = 0, kind = 0, momentum = 0;
+  int64_t tr = 0;
+  int32_t cw = 0, ntc = 0, ntr = 0, nfr = 0, nfc = 0;
+  bool empty = true;
+  // state slice offsets in bytes (SIZE_MAX: none)
+  size_t off_m = SIZE_MAX, off_v = SIZE_MAX, off_r = SIZE_MAX, off_c = SIZE_MAX;
+  // workspace offsets in bytes
+  size_t off_rowpart = SIZE_MAX, off_colpart = SIZE_MAX, off_ainv = SIZE_MAX, off_rsum = SIZE_MAX,
+         off_ssum = SIZE_MAX;
+};
+
+struct Plan {
+  std::vector<TensorPlan> t;
+  std::vector<Item> p1, fold, p2, p3;
+  size_t state_bytes = 0;
+  size_t ws_bytes = 0;
+  size_t off_table = 0, off_items = 0;   // workspace offsets of the device table and item lists
+};
+
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+
+// Validates the table and computes sizes, offsets and the work-item lists.
+int plan_build(const skew_tensor_desc *d, int n, Plan *out);
+
+// Kernel launchers (skew_kernels.hip). Return a hipError_t value.
+int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream);
+int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+
+}  // namespace skew

@@ -1,0 +1,107 @@
+// skew_plan.cpp -- host-only planning of a descriptor table: validation, the tier
+// state each tensor keeps (Fig. 1; Sec. 3 "The tiers"), the state size of Eq. 2
+// (plus the exact v of vectors, Table 6), the tile grid and the work-item lists.
+// No HIP calls: this runs without a GPU.
+#include <algorithm>
+#include <climits>
+#include <cmath>
+
+#include "skew_internal.h"
+
+namespace skew {
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
+  if (n < 0 || (n > 0 && d == nullptr) || out == nullptr) return SKEW_EINVAL;
+  Plan p;
+  p.t.resize(n);
+  size_t st = 0;        // state bytes
+  size_t ws_part = 0;   // partial-sum bytes (offsets relative to the partial region)
+  int64_t items_total = 0;
+  for (int i = 0; i < n; i++) {
+    const skew_tensor_desc &x = d[i];
+    TensorPlan &tp = p.t[i];
+    if (x.tier < SKEW_TIER_BACKBONE || x.tier > SKEW_TIER_ROUTER) return SKEW_EINVAL;
+    if (x.ndim != 1 && x.ndim != 2) return SKEW_EINVAL;
+    if (x.rows < 0 || x.cols < 0) return SKEW_EINVAL;
+    if (x.rows > 0 && x.cols > INT64_MAX / x.rows) return SKEW_EINVAL;
+    const int64_t N = x.rows * x.cols;
+    tp.tier = x.tier;
+    tp.N = N;
+    if (x.ndim == 1) {
+      if (N > 0 && x.rows != 1 && x.cols != 1) return SKEW_EINVAL;
+      tp.n = N > 0 ? 1 : 0;
+      tp.m = N;
+      tp.ld = N;
+    } else {
+      if (x.ld < x.cols || x.ld < 1) return SKEW_EINVAL;
+      if (x.rows > 0 && x.ld > INT64_MAX / x.rows) return SKEW_EINVAL;
+      tp.n = x.rows;
+      tp.m = x.cols;
+      tp.ld = x.ld;
+    }
+    tp.empty = (N == 0);
+    tp.kind = (x.tier == SKEW_TIER_ROUTER || x.ndim == 1) ? kExact : kFactored;
+    tp.momentum = (x.tier == SKEW_TIER_BACKBONE);
+    if (tp.empty) continue;
+
+    // state slices
+    if (tp.momentum) { tp.off_m = st; st = align_up(st + (size_t)N * 4); }
+    if (tp.kind == kExact) { tp.off_v = st; st = align_up(st + (size_t)N * 4); }
+    if (tp.kind == kFactored) {
+      tp.off_r = st; st = align_up(st + (size_t)tp.n * 4);
+      tp.off_c = st; st = align_up(st + (size_t)tp.m * 4);
+    }
+
+    // tile grid: tr rows x (512 * cw) columns, about kTileElems elements
+    tp.cw = (int32_t)std::min<int64_t>(kMaxCw, ceil_div(tp.m, kChunk));
+    const int64_t tc = (int64_t)kChunk * tp.cw;
+    tp.tr = std::max<int64_t>(1, kTileElems / tc);
+    const int64_t ntc = ceil_div(tp.m, tc), ntr = ceil_div(tp.n, tp.tr);
+    if (ntc * ntr > INT32_MAX / 2) return SKEW_EINVAL;
+    tp.ntc = (int32_t)ntc;
+    tp.ntr = (int32_t)ntr;
+    const int64_t tiles = ntc * ntr;
+
+    tp.off_ssum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
+    if (tp.kind == kFactored) {
+      const int64_t nfr = ceil_div(tp.n, kFold), nfc = ceil_div(tp.m, kFold);
+      if (nfr + nfc > INT32_MAX / 2) return SKEW_EINVAL;
+      tp.nfr = (int32_t)nfr;
+      tp.nfc = (int32_t)nfc;
+      tp.off_rowpart = ws_part; ws_part = align_up(ws_part + (size_t)ntc * tp.n * 8);
+      tp.off_colpart = ws_part; ws_part = align_up(ws_part + (size_t)ntr * tp.m * 8);
+      tp.off_ainv = ws_part; ws_part = align_up(ws_part + (size_t)tp.n * 8);
+      tp.off_rsum = ws_part; ws_part = align_up(ws_part + (size_t)nfr * 8);
+      for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p1.push_back({i, k});
+      for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold.push_back({i, k});
+      items_total += tiles + nfr + nfc;
+    }
+    for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p2.push_back({i, k});
+    for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p3.push_back({i, k});
+    items_total += 2 * tiles;
+    if (items_total > INT32_MAX / 2) return SKEW_EINVAL;
+  }
+  p.state_bytes = st;
+  // workspace: [device tensor table][items p1|fold|p2|p3][partials]
+  size_t ws = 0;
+  p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
+  p.off_items = ws;
+  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + 1));
+  for (auto &tp : p.t) {
+    if (tp.empty) continue;
+    tp.off_ssum += ws;
+    if (tp.kind == kFactored) {
+      tp.off_rowpart += ws;
+      tp.off_colpart += ws;
+      tp.off_ainv += ws;
+      tp.off_rsum += ws;
+    }
+  }
+  p.ws_bytes = ws + ws_part;
+  *out = std::move(p);
+  return SKEW_OK;
+}
+
+}  // namespace skew

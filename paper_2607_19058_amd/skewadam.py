@@ -1,0 +1,193 @@
+"""ctypes binding of ``include/skewadam.h``: argument marshalling only.
+
+Every step of the optimizer runs in the HIP library ``libskewadam.so``. PyTorch
+supplies device memory (the caller's bf16 weights and gradients, and the state and
+workspace buffers this wrapper allocates) and the HIP stream. There is no fallback:
+without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Iterable, List, Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libskewadam.so")
+
+SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
+BACKBONE, EXPERT, ROUTER = 0, 1, 2
+TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
+ABI_VERSION = 1
+
+# names every build of the library exports (checked by the CPU test suite)
+EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
+           "skew_abi_version")
+
+
+class SkewError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {_strerror(status)} (status {status})")
+        self.status = status
+
+
+class TensorDesc(ctypes.Structure):
+    _fields_ = [
+        ("tier", ctypes.c_int32), ("ndim", ctypes.c_int32),
+        ("rows", ctypes.c_int64), ("cols", ctypes.c_int64), ("ld", ctypes.c_int64),
+        ("tensor_id", ctypes.c_uint64),
+        ("w", ctypes.c_void_p), ("g", ctypes.c_void_p),
+        ("m", ctypes.c_void_p), ("v", ctypes.c_void_p), ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
+    ]
+
+
+class HParams(ctypes.Structure):
+    _fields_ = [
+        ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+        ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float), ("flags", ctypes.c_int32),
+        ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
+    ]
+
+
+_LIB = None
+
+
+def lib():
+    """Load the in-tree HIP library; raise if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                               "g.build()'` (hipcc, gfx950); there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        L.skew_state_bytes.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t),
+                                       ctypes.POINTER(ctypes.c_size_t)]
+        L.skew_state_bytes.restype = ctypes.c_int
+        L.skew_state_init.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_void_p]
+        L.skew_state_init.restype = ctypes.c_int
+        L.skew_step.argtypes = [ctypes.c_void_p, ctypes.POINTER(HParams), ctypes.c_void_p]
+        L.skew_step.restype = ctypes.c_int
+        L.skew_destroy.argtypes = [ctypes.c_void_p]
+        L.skew_destroy.restype = None
+        L.skew_strerror.argtypes = [ctypes.c_int]
+        L.skew_strerror.restype = ctypes.c_char_p
+        L.skew_abi_version.restype = ctypes.c_int
+        if L.skew_abi_version() != ABI_VERSION:
+            raise RuntimeError("libskewadam.so ABI version mismatch")
+        _LIB = L
+    return _LIB
+
+
+def _strerror(status: int) -> str:
+    try:
+        return lib().skew_strerror(status).decode()
+    except Exception:  # the library itself may be what failed to load
+        return "status"
+
+
+def make_desc(tier: int, ndim: int, rows: int, cols: int, ld: int, tensor_id: int, w_ptr: int = 0,
+              g_ptr: int = 0) -> TensorDesc:
+    return TensorDesc(tier, ndim, rows, cols, ld, tensor_id & (2**64 - 1), w_ptr or None, g_ptr or None,
+                      None, None, None, None)
+
+
+def state_bytes(descs: Sequence[TensorDesc]):
+    """(state_bytes, workspace_bytes) for a descriptor table; host only, needs no GPU."""
+    arr = (TensorDesc * max(1, len(descs)))(*descs)
+    sb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    rc = lib().skew_state_bytes(arr, len(descs), ctypes.byref(sb), ctypes.byref(wb))
+    if rc != SKEW_OK:
+        raise SkewError(rc, "skew_state_bytes")
+    return sb.value, wb.value
+
+
+def _desc_for(tier: int, w, g, tensor_id: int) -> TensorDesc:
+    import torch
+    if w.dtype != torch.bfloat16 or g.dtype != torch.bfloat16:
+        raise TypeError("weights and gradients must be bfloat16")
+    if w.device.type != "cuda" or g.device != w.device:
+        raise TypeError("weights and gradients must live on the same HIP device")
+    if w.shape != g.shape or w.stride() != g.stride():
+        raise ValueError("weight and gradient must have the same shape and strides")
+    if w.dim() == 1:
+        if w.numel() > 1 and w.stride(0) != 1:
+            raise ValueError("vectors must be contiguous")
+        return make_desc(tier, 1, 1, w.shape[0], max(1, w.shape[0]), tensor_id, w.data_ptr(), g.data_ptr())
+    if w.dim() != 2:
+        raise ValueError("only vectors and matrices are supported")
+    n, m = w.shape
+    if m > 1 and w.stride(1) != 1:
+        raise ValueError("matrices must be row-major (unit column stride)")
+    ld = w.stride(0) if n > 1 else max(1, m)
+    return make_desc(tier, 2, n, m, max(ld, m, 1), tensor_id, w.data_ptr(), g.data_ptr())
+
+
+class SkewAdam:
+    """One SkewAdam context over a fixed set of (tier, weight, gradient) tensors.
+
+    ``params`` is a list of ``(tier, w, g, tensor_id)`` with bf16 CUDA/HIP tensors.
+    The state and workspace are allocated here as torch byte tensors on the same
+    device; weights, gradients and these buffers must outlive the object.
+    """
+
+    def __init__(self, params: Iterable, stream=None):
+        import torch
+        params = list(params)
+        self._keep = params
+        self.descs = [_desc_for(TIERS.get(t, t), w, g, tid) for (t, w, g, tid) in params]
+        self.device = params[0][1].device if params else torch.device("cuda", torch.cuda.current_device())
+        sb, wb = state_bytes(self.descs)
+        self.state = torch.empty(max(sb, 1), dtype=torch.uint8, device=self.device)
+        self.workspace = torch.empty(max(wb, 1), dtype=torch.uint8, device=self.device)
+        self.state_nbytes, self.workspace_nbytes = sb, wb
+        self._arr = (TensorDesc * max(1, len(self.descs)))(*self.descs)
+        ctx = ctypes.c_void_p()
+        s = self._stream(stream)
+        rc = lib().skew_state_init(ctypes.byref(ctx), self._arr, len(self.descs), self.state.data_ptr(),
+                                   self.state.numel(), self.workspace.data_ptr(), self.workspace.numel(), s)
+        if rc != SKEW_OK:
+            raise SkewError(rc, "skew_state_init")
+        self._ctx = ctx
+        self._lib = lib()
+
+    @staticmethod
+    def _stream(stream) -> Optional[int]:
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+    def step(self, step: int, lr: float = 3e-4, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+             clip_threshold: float = 1.0, seed: int = 0, stream=None) -> None:
+        hp = HParams(lr, beta1, beta2, eps, clip_threshold, 0, int(step), int(seed) & (2**64 - 1))
+        rc = self._lib.skew_step(self._ctx, ctypes.byref(hp), self._stream(stream))
+        if rc != SKEW_OK:
+            raise SkewError(rc, "skew_step")
+
+    def state_views(self, i: int) -> dict:
+        """float32 torch views of tensor i's state slices (m, v, r, c; absent ones omitted)."""
+        import torch
+        d = self._arr[i]
+        n, m = (1, d.rows * d.cols) if d.ndim == 1 else (d.rows, d.cols)
+        shape = {"m": (n * m,), "v": (n * m,), "r": (n,), "c": (m,)}
+        base = self.state.data_ptr()
+        out = {}
+        for name in ("m", "v", "r", "c"):
+            p = getattr(d, name)
+            if p:
+                off = p - base
+                cnt = shape[name][0]
+                out[name] = self.state[off:off + 4 * cnt].view(torch.float32)
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "_ctx", None):
+            self._lib.skew_destroy(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,116 @@
+"""CPU checks of the C-ABI library: it loads without a GPU, exports every function
+declared in include/skewadam.h, validates descriptor tables, and sizes state as the
+closed-form model of Eq. 2 (plus the vectors' exact v) says."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2607_19058_amd as P
+from paper_2607_19058_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "skewadam.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|void|const char\s*\*)\s*\*?\s*(skew_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    names = _declared()
+    assert set(names) == set(P.skewadam.EXPORTS)
+    L = ctypes.CDLL(P.skewadam.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    assert P.lib().skew_abi_version() == 1
+    for code in (0, -1, -2, -3, -4, -99):
+        assert P.lib().skew_strerror(code)
+
+
+def _descs(wl):
+    out = []
+    for s in wl.specs:
+        if len(s.shape) == 1:
+            out.append(P.make_desc(s.tier, 1, 1, s.shape[0], s.shape[0], s.tensor_id))
+        else:
+            out.append(P.make_desc(s.tier, 2, s.shape[0], s.shape[1], s.shape[1], s.tensor_id))
+    return out
+
+
+def _slices(wl):
+    n = 0
+    for s in wl.specs:
+        exact = s.tier == W.ROUTER or len(s.shape) == 1
+        n += (s.tier == W.BACKBONE) + (1 if exact else 2)
+    return n
+
+
+@pytest.mark.parametrize("name", ["tiny", "layer", "full", "ragged"])
+def test_state_bytes_match_closed_form(name):
+    wl = W.get(name)
+    sb, wb = P.state_bytes(_descs(wl))
+    closed = oracle.state_bytes([(s.tier, s.shape) for s in wl.specs])
+    assert closed <= sb <= closed + 256 * _slices(wl)
+    assert wb > 0
+    if name == "full":
+        assert closed == 1_384_279_040          # 1.289 GiB for the 6.78B synthetic set
+        assert wb < 0.02 * 12.64 * 2**30        # partial sums stay a small fraction of G
+
+
+def test_paper_inventory_state_bytes():
+    inv = []
+    for line in open(os.path.join(ROOT, "tests", "golden", "paper_model_inventory.txt")):
+        line = line.split("|")[0].strip()
+        if line and not line.startswith("#"):
+            tier, count, shape = line.split()
+            inv += [(oracle.TIER_NAMES[tier], tuple(int(x) for x in shape.split("x")))] * int(count)
+    descs = []
+    for k, (t, s) in enumerate(inv):
+        if len(s) == 1:
+            descs.append(P.make_desc(t, 1, 1, s[0], s[0], k))
+        else:
+            descs.append(P.make_desc(t, 2, s[0], s[1], s[1], k))
+    sb, _ = P.state_bytes(descs)
+    assert 1_380_800_000 <= sb <= 1_380_800_000 + 256 * 3 * len(inv)
+    assert round(sb / 2**30, 2) == 1.29      # Table 1, Table 6
+
+
+def _rc(descs):
+    arr = (P.TensorDesc * max(1, len(descs)))(*descs)
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    return P.lib().skew_state_bytes(arr, len(descs), ctypes.byref(a), ctypes.byref(b))
+
+
+def test_validation_errors():
+    ok = P.make_desc(1, 2, 4, 8, 8, 0)
+    assert _rc([ok]) == 0
+    assert _rc([P.make_desc(3, 2, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL        # unknown tier
+    assert _rc([P.make_desc(-1, 2, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL
+    assert _rc([P.make_desc(1, 3, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL        # ndim 3
+    assert _rc([P.make_desc(1, 2, 4, 8, 7, 0)]) == P.skewadam.SKEW_EINVAL        # ld < cols
+    assert _rc([P.make_desc(1, 2, -1, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL       # negative rows
+    assert _rc([P.make_desc(1, 1, 2, 3, 3, 0)]) == P.skewadam.SKEW_EINVAL        # vector that is 2x3
+    assert _rc([P.make_desc(1, 2, 1 << 40, 1 << 30, 1 << 30, 0)]) == P.skewadam.SKEW_EINVAL  # overflow
+    assert P.lib().skew_state_bytes(None, -1, None, None) == P.skewadam.SKEW_EINVAL
+
+
+def test_empty_and_large_descriptors():
+    # tensors with no elements are accepted and keep no state
+    assert P.state_bytes([P.make_desc(1, 2, 0, 8, 8, 0), P.make_desc(0, 1, 1, 0, 1, 1)])[0] == 0
+    assert P.state_bytes([])[0] == 0
+    # more than 2^31 elements: 64-bit sizes throughout
+    sb, wb = P.state_bytes([P.make_desc(1, 2, 65537, 32768, 32768, 0)])
+    assert sb >= 4 * (65537 + 32768)
+    sb, _ = P.state_bytes([P.make_desc(2, 1, 1, (1 << 31) + 5, (1 << 31) + 5, 0)])
+    assert sb >= 4 * ((1 << 31) + 5)
+
+
+def test_binding_refuses_missing_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(P.skewadam, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(P.skewadam, "_LIB", None)
+    with pytest.raises(RuntimeError):
+        P.skewadam.lib()

@@ -1,0 +1,170 @@
+"""GPU parity: the HIP step against the CPU oracle on the same seeded inputs.
+
+Workloads: the tiny one-layer MoE on every tensor, unit shapes (odd, ragged, strided,
+unaligned, vectors), and the full-size workloads (one MoE layer at width 2048, the
+heavy-tailed stress case, the ragged tier mix, and the 6.78B parameter set) on
+sampled tensors. Every test calls the library through its C ABI.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_19058_amd import SkewAdam
+from paper_2607_19058_amd import workloads as W
+
+from parity_util import ParityRun, bits, log, run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a HIP device")
+    torch.cuda.init()
+
+
+def test_tiny_every_tensor():
+    log("[parity] tiny: 21 tensors, 10 steps, all compared")
+    st = run(W.get("tiny"))
+    assert st.ok(), st
+
+
+def _unit_workload():
+    specs = []
+    shapes = [(1, 1), (1, 7), (7, 1), (3, 5), (13, 17), (256, 8), (64, 520), (33, 1031), (5,), (1,), (4097,),
+              (2, 2048), (300, 2056)]
+    for tier in (W.BACKBONE, W.EXPERT, W.ROUTER):
+        for sh in shapes:
+            specs.append(W.Spec(f"t{tier}_{'x'.join(map(str, sh))}", tier, sh, len(specs)))
+    return W.Workload("unit", specs, 3)
+
+
+def test_unit_shapes_all_tiers():
+    log("[parity] unit shapes: odd, ragged and vector shapes in every tier, 3 steps")
+    st = run(_unit_workload(), hp=dict(oracle.DEFAULTS, lr=1e-2))
+    assert st.ok(), st
+
+
+def test_strided_and_unaligned_tensors():
+    """Row stride larger than the width, and pointers off 16-byte alignment: the
+    scalar path must give the same bits as the oracle on the dense copy."""
+    log("[parity] strided / unaligned tensors")
+    dev = torch.device("cuda")
+    wl = W.Workload("strided", [W.Spec("a", W.EXPERT, (37, 200), 0), W.Spec("b", W.BACKBONE, (64, 1024), 1),
+                                W.Spec("c", W.ROUTER, (16, 24), 2)], 3)
+    bases, Ws, Gs = [], [], []
+    for s, pad, off in zip(wl.specs, (56, 8, 3), (0, 1, 1)):
+        n, m = s.shape
+        wb = torch.zeros((n, m + pad + off), dtype=torch.bfloat16, device=dev)
+        gb = torch.zeros_like(wb)
+        w = wb[:, off:off + m]
+        w.copy_(W.init_weight(s, wl, dev))
+        bases.append((wb, gb))
+        Ws.append(w)
+        Gs.append(gb[:, off:off + m])
+    opt = SkewAdam([(s.tier, Ws[k], Gs[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+    O = [oracle.Tensor(tier=s.tier, w=bits(Ws[k]).copy(), g=np.zeros(s.shape, np.uint16),
+                       tensor_id=s.tensor_id).init_state() for k, s in enumerate(wl.specs)]
+    for t in range(1, 4):
+        for k, s in enumerate(wl.specs):
+            g = torch.empty(s.shape, dtype=torch.bfloat16, device=dev)
+            W.fill_grad(s, wl, t, g)
+            Gs[k].copy_(g)
+            O[k].g = bits(g)
+        opt.step(t, lr=1e-2)
+        oracle.step(O, t, lr=1e-2, want_y=True)
+        torch.cuda.synchronize()
+        for k, s in enumerate(wl.specs):
+            gw = bits(Ws[k])
+            diff = gw != O[k].w
+            if diff.any():
+                from parity_util import near_boundary
+                assert near_boundary(O[k].y_out[diff]).all(), (s.name, t, int(diff.sum()))
+            assert diff.mean() <= 1e-3, (s.name, t)
+            # padding columns are untouched
+            wb, gb = bases[k]
+            n, m = s.shape
+            assert torch.count_nonzero(wb[:, :(0, 1, 1)[k]]) == 0
+            assert torch.count_nonzero(wb[:, (0, 1, 1)[k] + m:]) == 0
+
+
+def test_layer_sampled():
+    wl = W.get("layer")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sc = W.expert_scales(wl, 1)[0]
+    zero_e = int(np.flatnonzero(sc == 0)[0])
+    small_e = int(np.argsort(np.where(sc > 0, sc, np.inf))[0])
+    big_e = int(np.argmax(sc))
+    sample = [names["attn.0"], names["ffn.down"], names[f"ex{zero_e}.up"], names[f"ex{small_e}.down"],
+              names[f"ex{big_e}.up"], names["ex7.down"], names["router"]]
+    log(f"[parity] layer: 263 tensors (4.35B params), 5 steps, sampled {sample}")
+    st = run(wl, sample=sample)
+    assert st.ok(), st
+
+
+def test_stress_sampled():
+    wl = W.get("stress")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sample = [names["attn.1"], names["ffn.up"], names["ex3.up"], names["ex64.down"], names["router"]]
+    log(f"[parity] stress: Student-t(2) gradients with outliers and 90% sparse experts, sampled {sample}")
+    st = run(wl, sample=sample)
+    assert st.ok(), st
+
+
+def test_determinism_order_and_resume():
+    """Bit-identical across runs, descriptor orders and a checkpoint/resume split."""
+    log("[parity] determinism, descriptor order, resume")
+    dev = torch.device("cuda")
+    wl = W.get("tiny")
+    G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
+
+    def run_steps(order, t_from, t_to, Wt, opt=None):
+        if opt is None:
+            opt = SkewAdam([(wl.specs[k].tier, Wt[k], G[k], wl.specs[k].tensor_id) for k in order])
+        for t in range(t_from, t_to + 1):
+            sc = W.expert_scales(wl, t)
+            for k, s in enumerate(wl.specs):
+                W.fill_grad(s, wl, t, G[k], sc)
+            opt.step(t, seed=5)
+        torch.cuda.synchronize()
+        return opt
+
+    def fresh():
+        return [W.init_weight(s, wl, dev) for s in wl.specs]
+
+    Wa = fresh()
+    a = run_steps(list(range(len(wl.specs))), 1, 10, Wa)
+    Wb = fresh()
+    run_steps(list(range(len(wl.specs))), 1, 10, Wb)
+    Wc = fresh()
+    run_steps(list(reversed(range(len(wl.specs)))), 1, 10, Wc)
+    Wd = fresh()
+    d = run_steps(list(range(len(wl.specs))), 1, 5, Wd)
+    saved = d.state.clone()
+    d.close()
+    d2 = SkewAdam([(s.tier, Wd[k], G[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+    d2.state.copy_(saved)
+    run_steps(None, 6, 10, Wd, opt=d2)
+    for k in range(len(wl.specs)):
+        assert torch.equal(Wa[k].view(torch.int16), Wb[k].view(torch.int16)), "run to run"
+        assert torch.equal(Wa[k].view(torch.int16), Wc[k].view(torch.int16)), "descriptor order"
+        assert torch.equal(Wa[k].view(torch.int16), Wd[k].view(torch.int16)), "resume"
+    assert torch.equal(a.state, d2.state)
+
+
+def test_hparam_errors_launch_nothing():
+    dev = torch.device("cuda")
+    w = torch.ones((4, 8), dtype=torch.bfloat16, device=dev)
+    g = torch.ones_like(w)
+    opt = SkewAdam([(W.EXPERT, w, g, 0)])
+    from paper_2607_19058_amd import SkewError
+    for bad in (dict(step=0), dict(step=1, eps=0.0), dict(step=1, beta2=1.0), dict(step=1, beta1=-0.1),
+                dict(step=1, clip_threshold=0.0), dict(step=1, lr=float("nan"))):
+        with pytest.raises(SkewError):
+            opt.step(**bad)
+    torch.cuda.synchronize()
+    assert torch.equal(w, torch.ones_like(w))

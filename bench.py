@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Benchmark of the SkewAdam optimizer step on one MI355X.
+
+Workload: the full 6,784,327,680-parameter synthetic MoE parameter set (432 tensors:
+backbone 341,352,448 / experts 6,442,450,944 / router 524,288 parameters, the tier
+sizes of the paper's model), bf16 weights and gradients resident in HBM.
+
+One timed step is one call of skew_step over every tensor, i.e. the whole hot path
+(pass-1 sums, fold, pass-2 sum of squares, pass-3 update and dithered write-back).
+W warmup steps draw fresh seeded gradients; the K timed steps then run back to back
+on the resident gradient of one further draw, with the step counter advancing, so
+inputs are in HBM when the timed region starts. Prints one JSON line.
+
+Reported alongside the headline (parameters updated per second):
+  roofline      the dominant kernel's achieved algorithmic GB/s against 8 TB/s, from
+                HIP events recorded around each of the library's kernels on the launch
+                stream over the timed region; `traffic` from the committed rocprofv3
+                FETCH_SIZE / WRITE_SIZE summary when the kernel source still matches it
+  step          the whole step's algorithmic bytes and effective GB/s
+  cpu_baseline  the CPU oracle (plain C, OpenMP) on a bounded resident sample of the
+                same workload, on this host's cores
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Gparams/s per SkewAdam step + achieved HBM GB/s (% of peak), 6.78B MoE"
+PEAK_GBPS = 8000.0
+# Algorithmic bytes per parameter and tier: G read 2, W read + write 4, fp32 M read + write 8,
+# fp32 exact V read + write 8 (the factored R, C and per-tensor scalars are negligible).
+BYTES_PER_PARAM = {"expert": 6, "backbone_matrix": 14, "backbone_vector": 22, "router": 14,
+                   "expert_vector": 14, "router_vector": 14}
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_19058_amd", "csrc", "skew_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_full.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def tier_class(spec) -> str:
+    from paper_2607_19058_amd import workloads as W
+    vec = len(spec.shape) == 1
+    if spec.tier == W.EXPERT:
+        return "expert_vector" if vec else "expert"
+    if spec.tier == W.ROUTER:
+        return "router_vector" if vec else "router"
+    return "backbone_vector" if vec else "backbone_matrix"
+
+
+def algorithmic_bytes(specs) -> int:
+    return sum(BYTES_PER_PARAM[tier_class(s)] * s.numel for s in specs)
+
+
+def kernel_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
+    """The CPU oracle as it stands, on a resident sample of the workload: 8 expert
+    matrices, one attention matrix, one norm vector and one router, stepped repeatedly."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2607_19058_amd import workloads as W
+    ex = [s for s in wl.specs if s.tier == W.EXPERT][:8]
+    bb = [s for s in wl.specs if s.tier == W.BACKBONE and len(s.shape) == 2 and s.shape == (2048, 2048)][:1]
+    vec = [s for s in wl.specs if s.tier == W.BACKBONE and len(s.shape) == 1][:1]
+    rt = [s for s in wl.specs if s.tier == W.ROUTER][:1]
+    sample = ex + bb + vec + rt
+    T = []
+    for s in sample:
+        w = W.init_weight(s, wl, "cpu").view(torch.int16).numpy().view(np.uint16).copy()
+        g = torch.empty(s.shape, dtype=torch.bfloat16)
+        W.fill_grad(s, wl, 1, g)
+        T.append(oracle.Tensor(tier=s.tier, w=w, g=g.view(torch.int16).numpy().view(np.uint16).copy(),
+                               tensor_id=s.tensor_id).init_state())
+    params = sum(s.numel for s in sample)
+    t0 = time.perf_counter()
+    steps = 0
+    while True:
+        steps += 1
+        oracle.step(T, steps)
+        if time.perf_counter() - t0 >= budget_s or steps >= 40:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(params * steps / dt / 1e9, 4), "unit": "Gparams/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"{len(sample)} tensors of the full workload ({params:,} params: 8 expert matrices, "
+                      f"one 2048x2048 attention matrix, one norm vector, one router), {steps} steps, "
+                      f"{dt:.1f} s wall on {oracle.threads()} OpenMP threads"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="full")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "
+              "the optimizer step is measured on one MI355X's share", file=sys.stderr, flush=True)
+        return 2
+
+    import torch
+    from paper_2607_19058_amd import SkewAdam
+    from paper_2607_19058_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a HIP device")
+        return 1
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    wl = W.get(args.workload)
+    log(f"[bench] workload {wl.name}: {len(wl.specs)} tensors, {wl.numel:,} params; allocating")
+    Wt = [W.init_weight(s, wl, dev) for s in wl.specs]
+    G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
+    opt = SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+
+    def draw(t):
+        sc = W.expert_scales(wl, t)
+        for k, s in enumerate(wl.specs):
+            W.fill_grad(s, wl, t, G[k], sc)
+
+    hp = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0, seed=0)
+    for t in range(1, args.warmup + 1):
+        draw(t)
+        opt.step(t, **hp)
+    draw(args.warmup + 1)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
+
+    opt.timing_enable(args.steps)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for j in range(args.steps):
+        opt.step(args.warmup + 1 + j, **hp)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel = opt.timing_read()
+    steps_rec = per_kernel.pop("_steps")
+    ev_ms = e0.elapsed_time(e1)
+
+    ms_per_step = 1e3 * wall / args.steps
+    params = wl.numel
+    alg = algorithmic_bytes(wl.specs)
+    kern_avg = {k: v / max(1, steps_rec) for k, v in per_kernel.items()}
+    dom = max(kern_avg, key=kern_avg.get)
+    # the apply kernel alone reads G, W (and M or V) and writes W (and M or V) once:
+    # its algorithmic bytes per launch are the step's; the other kernels re-read G
+    dom_bytes = {"p3_apply_dither": alg,
+                 "p1_rowcol_sumsq": 2 * sum(s.numel for s in wl.specs if tier_class(s) in ("expert", "backbone_matrix")),
+                 "p2_update_sumsq": alg, "fold_rc_ema": 0}[dom]
+    achieved = dom_bytes / (kern_avg[dom] * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("kernel_src_sha") == kernel_sha() and tr.get("kernel") == dom and tr.get("workload") == wl.name:
+            traffic = tr.get("hbm_bytes_per_launch")
+    roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_GBPS, 4), "traffic": traffic,
+            "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_ms": round(kern_avg[dom], 4)}
+    step_gbps = alg / (ms_per_step * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(params / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "Gparams/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {params:,}-parameter synthetic MoE parameter set, {len(wl.specs)} tensors "
+                               "(bf16 weights and gradients, fp32 state)",
+                   "params": params, "tensors": len(wl.specs), "state_bytes": opt.state_nbytes,
+                   "workspace_bytes": opt.workspace_nbytes},
+        "roofline": roof,
+        "step": {"algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3),
+                 "effective_GBps": round(step_gbps, 1), "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),
+                 "event_ms_per_step": round(ev_ms / args.steps, 4),
+                 "kernel_ms_per_step": {k: round(v, 4) for k, v in kern_avg.items()}},
+    }
+    if not args.no_cpu_baseline:
+        del Wt, G, opt
+        torch.cuda.empty_cache()
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -145,6 +145,20 @@ const char *skew_strerror(int status);
 /* SKEW_ABI_VERSION of the loaded library. */
 int skew_abi_version(void);
 
+/* ---- Diagnostics: per-launch timing (not part of the step's definition) ----
+ * skew_timing_enable(ctx, max_steps) creates HIP events for up to max_steps later
+ * calls of skew_step on ctx, which then record one event before its first kernel and
+ * one after each kernel on the step's stream (no synchronisation, no work skipped).
+ * max_steps = 0 frees the events and stops recording. Errors: SKEW_EINVAL, SKEW_EHIP.
+ * skew_timing_read(ctx, ms, max_launches, launches, steps) waits for the recorded
+ * events, writes into ms[j] (host array of max_launches doubles) the summed duration
+ * in milliseconds of the step's j-th kernel over the recorded steps, sets *launches
+ * to the number of kernels per step and *steps to the number of steps recorded, and
+ * restarts recording. skew_launch_name(ctx, j) names kernel j (static string). */
+int skew_timing_enable(skew_ctx *ctx, int max_steps);
+int skew_timing_read(skew_ctx *ctx, double *ms, int max_launches, int *launches, int *steps);
+const char *skew_launch_name(skew_ctx *ctx, int j);
+
 #ifdef __cplusplus
 }
 #endif

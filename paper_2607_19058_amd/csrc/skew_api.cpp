@@ -11,10 +11,22 @@
 
 using namespace skew;
 
+namespace {
+constexpr int kLaunches = 4;
+const char *const kLaunchNames[kLaunches] = {"p1_rowcol_sumsq", "fold_rc_ema", "p2_update_sumsq",
+                                             "p3_apply_dither"};
+}  // namespace
+
 struct skew_ctx {
   Plan plan;
   DevTensor *d_table = nullptr;
   Item *d_p1 = nullptr, *d_fold = nullptr, *d_p2 = nullptr, *d_p3 = nullptr;
+  // diagnostics: events [step][kLaunches + 1]
+  std::vector<hipEvent_t> ev;
+  int ev_steps = 0, ev_used = 0;
+  ~skew_ctx() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
 };
 
 namespace {
@@ -169,11 +181,62 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
   const StepConsts k = make_consts(*hp);
   const Plan &p = ctx->plan;
-  int e = launch_p1(ctx->d_table, ctx->d_p1, (int64_t)p.p1.size(), stream);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t *ev = nullptr;
+  if (ctx->ev_used < ctx->ev_steps) ev = &ctx->ev[(size_t)ctx->ev_used++ * (kLaunches + 1)];
+  int e = ev ? (int)hipEventRecord(ev[0], s) : 0;
+  if (e == 0) e = launch_p1(ctx->d_table, ctx->d_p1, (int64_t)p.p1.size(), stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[1], s);
   if (e == 0) e = launch_fold(ctx->d_table, ctx->d_fold, (int64_t)p.fold.size(), k, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[2], s);
   if (e == 0) e = launch_p2(ctx->d_table, ctx->d_p2, (int64_t)p.p2.size(), k, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[3], s);
   if (e == 0) e = launch_p3(ctx->d_table, ctx->d_p3, (int64_t)p.p3.size(), k, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[4], s);
   return e == 0 ? SKEW_OK : SKEW_EHIP;
+}
+
+int skew_timing_enable(skew_ctx *ctx, int max_steps) {
+  if (ctx == nullptr || max_steps < 0) return SKEW_EINVAL;
+  for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
+  ctx->ev.clear();
+  ctx->ev_steps = ctx->ev_used = 0;
+  const size_t n = (size_t)max_steps * (kLaunches + 1);
+  ctx->ev.reserve(n);
+  for (size_t i = 0; i < n; i++) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (hipEvent_t x : ctx->ev) (void)hipEventDestroy(x);
+      ctx->ev.clear();
+      return SKEW_EHIP;
+    }
+    ctx->ev.push_back(e);
+  }
+  ctx->ev_steps = max_steps;
+  return SKEW_OK;
+}
+
+int skew_timing_read(skew_ctx *ctx, double *ms, int max_launches, int *launches, int *steps) {
+  if (ctx == nullptr || ms == nullptr || max_launches < kLaunches) return SKEW_EINVAL;
+  for (int j = 0; j < kLaunches; j++) ms[j] = 0.0;
+  for (int st = 0; st < ctx->ev_used; st++) {
+    hipEvent_t *ev = &ctx->ev[(size_t)st * (kLaunches + 1)];
+    if (hipEventSynchronize(ev[kLaunches]) != hipSuccess) return SKEW_EHIP;
+    for (int j = 0; j < kLaunches; j++) {
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, ev[j], ev[j + 1]) != hipSuccess) return SKEW_EHIP;
+      ms[j] += t;
+    }
+  }
+  if (launches) *launches = kLaunches;
+  if (steps) *steps = ctx->ev_used;
+  ctx->ev_used = 0;
+  return SKEW_OK;
+}
+
+const char *skew_launch_name(skew_ctx *ctx, int j) {
+  (void)ctx;
+  return (j >= 0 && j < kLaunches) ? kLaunchNames[j] : "";
 }
 
 void skew_destroy(skew_ctx *ctx) { delete ctx; }

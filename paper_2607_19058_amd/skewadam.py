@@ -21,7 +21,7 @@ ABI_VERSION = 1
 
 # names every build of the library exports (checked by the CPU test suite)
 EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
-           "skew_abi_version")
+           "skew_abi_version", "skew_timing_enable", "skew_timing_read", "skew_launch_name")
 
 
 class SkewError(RuntimeError):
@@ -73,6 +73,13 @@ def lib():
         L.skew_strerror.argtypes = [ctypes.c_int]
         L.skew_strerror.restype = ctypes.c_char_p
         L.skew_abi_version.restype = ctypes.c_int
+        L.skew_timing_enable.argtypes = [ctypes.c_void_p, ctypes.c_int]
+        L.skew_timing_enable.restype = ctypes.c_int
+        L.skew_timing_read.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]
+        L.skew_timing_read.restype = ctypes.c_int
+        L.skew_launch_name.argtypes = [ctypes.c_void_p, ctypes.c_int]
+        L.skew_launch_name.restype = ctypes.c_char_p
         if L.skew_abi_version() != ABI_VERSION:
             raise RuntimeError("libskewadam.so ABI version mismatch")
         _LIB = L
@@ -164,6 +171,23 @@ class SkewAdam:
         rc = self._lib.skew_step(self._ctx, ctypes.byref(hp), self._stream(stream))
         if rc != SKEW_OK:
             raise SkewError(rc, "skew_step")
+
+    def timing_enable(self, max_steps: int) -> None:
+        """Record HIP events around each of the library's kernels for the next max_steps steps."""
+        rc = self._lib.skew_timing_enable(self._ctx, int(max_steps))
+        if rc != SKEW_OK:
+            raise SkewError(rc, "skew_timing_enable")
+
+    def timing_read(self) -> dict:
+        """{kernel name: summed milliseconds} over the recorded steps, plus '_steps'."""
+        ms = (ctypes.c_double * 16)()
+        nl, ns = ctypes.c_int(), ctypes.c_int()
+        rc = self._lib.skew_timing_read(self._ctx, ms, 16, ctypes.byref(nl), ctypes.byref(ns))
+        if rc != SKEW_OK:
+            raise SkewError(rc, "skew_timing_read")
+        out = {self._lib.skew_launch_name(self._ctx, j).decode(): ms[j] for j in range(nl.value)}
+        out["_steps"] = ns.value
+        return out
 
     def state_views(self, i: int) -> dict:
         """float32 torch views of tensor i's state slices (m, v, r, c; absent ones omitted)."""

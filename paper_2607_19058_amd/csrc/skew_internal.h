@@ -13,7 +13,7 @@ enum Kind : int32_t { kFactored = 0, kExact = 1 };
 constexpr int kThreads = 256;           // threads per work-group (4 wave64)
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 512;             // columns one wave covers with one 16-byte load per lane
-constexpr int kMaxCw = 4;               // at most 4 chunks (2048 columns) per tile row
+constexpr int kMaxCw = 4;               // chunks per tile row: 1, 2 or 4 (at most 2048 columns)
 constexpr int kFold = 256;              // rows (or columns) folded by one work-group
 constexpr int64_t kTileElems = 1 << 19; // target elements per tile: 1 MiB of bf16 gradient
 constexpr size_t kAlign = 256;
@@ -30,7 +30,7 @@ struct DevTensor {
   double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
   int64_t n, m, ld;       // rows, columns, row stride (elements)
   int64_t tr;             // rows per tile
-  int32_t cw;             // 512-column chunks per tile (1..4)
+  int32_t cw;             // 512-column chunks per tile (1, 2 or 4)
   int32_t ntc, ntr;       // column strips, row bands
   int32_t nfr, nfc;       // fold work-groups over rows, over columns
   int32_t kind;           // kFactored / kExact

@@ -22,6 +22,35 @@
 namespace skew {
 namespace {
 
+// Tensor pointers come from the device-resident table, so the compiler cannot infer
+// their address space; these accessors make every data access a global (not flat) one.
+template <class T>
+__device__ __forceinline__ T ldg(const T *p) {
+  return *(const __attribute__((address_space(1))) T *)p;
+}
+template <class T>
+__device__ __forceinline__ void stg(T *p, T v) {
+  *(__attribute__((address_space(1))) T *)p = v;
+}
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg(const uint4 *p) {
+  const u32x4_t v = ldg(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 ldg(const float4 *p) {
+  const f32x4_t v = ldg(reinterpret_cast<const f32x4_t *>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void stg(uint4 *p, uint4 v) {
+  const u32x4_t u = {v.x, v.y, v.z, v.w};
+  stg(reinterpret_cast<u32x4_t *>(p), u);
+}
+__device__ __forceinline__ void stg(float4 *p, float4 v) {
+  const f32x4_t u = {v.x, v.y, v.z, v.w};
+  stg(reinterpret_cast<f32x4_t *>(p), u);
+}
+
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 __device__ __forceinline__ float bf_one(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -103,18 +132,53 @@ __device__ __forceinline__ double block_sum(double x, double *sh) {
   return r;
 }
 
+// A tile is one row band (rows band, band + ntr, band + 2 ntr, ...: interleaved, so that
+// the work-groups running at the same time on one tensor read neighbouring rows) times
+// one column strip of 512*cw columns.
 struct Tile {
-  int64_t r0, r1, c0;
+  int64_t nr, c0, stride;   // local rows, first column, row stride between local rows
   int band, strip;
+  __device__ __forceinline__ int64_t row(int64_t lr) const { return band + lr * stride; }
 };
 __device__ __forceinline__ Tile tile_of(const DevTensor &t, int tile) {
   Tile g;
   g.band = tile / t.ntc;
   g.strip = tile - g.band * t.ntc;
-  g.r0 = (int64_t)g.band * t.tr;
-  g.r1 = min(t.n, g.r0 + t.tr);
+  g.stride = t.ntr;
+  g.nr = (t.n - g.band + t.ntr - 1) / t.ntr;
   g.c0 = (int64_t)g.strip * kChunk * t.cw;
   return g;
+}
+
+// Wave -> (chunk, row) map inside a tile: the cw chunks of a row go to cw adjacent waves,
+// so one work-group iteration reads kWaves / cw whole tile rows (up to 4 KB contiguous),
+// and every wave keeps the same 512 columns for the whole tile.
+struct WaveMap {
+  int wq, wr, rpi, lane;
+  int64_t col;   // first of the lane's 8 columns
+  __device__ __forceinline__ WaveMap(const DevTensor &t, const Tile &tl) {
+    const int wave = threadIdx.x >> 6;
+    lane = threadIdx.x & 63;
+    wq = wave % t.cw;
+    wr = wave / t.cw;
+    rpi = kWaves / t.cw;
+    col = tl.c0 + (int64_t)wq * kChunk + lane * 8;
+  }
+};
+
+__device__ __forceinline__ void load_g8(const DevTensor &t, int64_t i, int64_t col, float *g) {
+  const uint16_t *row = t.g + i * t.ld;
+  if (t.vec) {
+    if (col < t.m) {
+      unpack8(ldg(reinterpret_cast<const uint4 *>(row + col)), g);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; e++) g[e] = 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; e++) g[e] = (col + e < t.m) ? bf_one(ldg(row + col + e)) : 0.f;
+  }
 }
 
 // --------------------------------------------------------------------------------------------
@@ -128,88 +192,62 @@ __device__ __forceinline__ double wave_sum_d(double x) {
   return x;
 }
 
+constexpr int kRowSlots = (int)(kTileElems / kChunk);   // tile rows x chunks per row
+
 __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restrict__ TT,
                                                       const Item *__restrict__ items) {
-  __shared__ double sh[2][kChunk * kMaxCw];
+  __shared__ double colsh[kWaves][kChunk];
+  __shared__ double rowsh[kRowSlots];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   const Tile tl = tile_of(t, it.tile);
-  const int64_t n = t.n, m = t.m, ld = t.ld;
+  const WaveMap wm(t, tl);
   const int cw = t.cw;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint16_t *__restrict__ G = t.g;
 
-  double acc[kMaxCw][8];
+  double acc[8];
 #pragma unroll
-  for (int q = 0; q < kMaxCw; q++)
+  for (int e = 0; e < 8; e++) acc[e] = 0.0;
+  for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
+    const bool two = lr + wm.rpi < tl.nr;
+    float ga[8], gb[8];
+    load_g8(t, tl.row(lr), wm.col, ga);
+    if (two) load_g8(t, tl.row(lr + wm.rpi), wm.col, gb);
+    double ra = 0.0, rb = 0.0;
 #pragma unroll
-    for (int e = 0; e < 8; e++) acc[q][e] = 0.0;
-
-  for (int64_t i = tl.r0 + wave; i < tl.r1; i += kWaves) {
-    const uint16_t *row = G + i * ld;
-    double rs = 0.0;
-#pragma unroll
-    for (int q = 0; q < kMaxCw; q++) {
-      if (q < cw) {
-        const int64_t col = tl.c0 + q * kChunk + lane * 8;
-        float g[8];
-        if (t.vec) {
-          if (col < m) {
-            unpack8(*reinterpret_cast<const uint4 *>(row + col), g);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 8; e++) g[e] = 0.f;
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; e++) g[e] = (col + e < m) ? bf_one(row[col + e]) : 0.f;
-        }
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-          const double gd = (double)g[e];
-          rs = fma(gd, gd, rs);
-          acc[q][e] = fma(gd, gd, acc[q][e]);
-        }
-      }
+    for (int e = 0; e < 8; e++) {
+      const double x = (double)ga[e];
+      ra = fma(x, x, ra);
+      acc[e] = fma(x, x, acc[e]);
     }
-    rs = wave_sum_d(rs);
-    if (lane == 0) t.rowpart[(int64_t)tl.strip * n + i] = rs;
-  }
-  // column partials of the four waves: (w0 + w2) + (w1 + w3)
-  if (wave >= 2) {
-#pragma unroll
-    for (int q = 0; q < kMaxCw; q++)
-      if (q < cw)
-#pragma unroll
-        for (int e = 0; e < 8; e++) sh[wave - 2][q * kChunk + lane * 8 + e] = acc[q][e];
-  }
-  __syncthreads();
-  if (wave < 2) {
-#pragma unroll
-    for (int q = 0; q < kMaxCw; q++)
-      if (q < cw)
-#pragma unroll
-        for (int e = 0; e < 8; e++) acc[q][e] += sh[wave][q * kChunk + lane * 8 + e];
-  }
-  __syncthreads();
-  if (wave == 1) {
-#pragma unroll
-    for (int q = 0; q < kMaxCw; q++)
-      if (q < cw)
-#pragma unroll
-        for (int e = 0; e < 8; e++) sh[0][q * kChunk + lane * 8 + e] = acc[q][e];
-  }
-  __syncthreads();
-  if (wave == 0) {
-#pragma unroll
-    for (int q = 0; q < kMaxCw; q++) {
-      if (q >= cw) continue;
+    if (two) {
 #pragma unroll
       for (int e = 0; e < 8; e++) {
-        const int64_t col = tl.c0 + q * kChunk + lane * 8 + e;
-        if (col < m) t.colpart[(int64_t)tl.band * m + col] = acc[q][e] + sh[0][q * kChunk + lane * 8 + e];
+        const double x = (double)gb[e];
+        rb = fma(x, x, rb);
+        acc[e] = fma(x, x, acc[e]);
       }
     }
+    ra = wave_sum_d(ra);
+    rb = wave_sum_d(rb);
+    if (wm.lane == 0) {
+      rowsh[lr * cw + wm.wq] = ra;
+      if (two) rowsh[(lr + wm.rpi) * cw + wm.wq] = rb;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; e++) colsh[threadIdx.x >> 6][wm.lane * 8 + e] = acc[e];
+  __syncthreads();
+  for (int r = threadIdx.x; r < (int)tl.nr; r += kThreads) {
+    double s = 0.0;
+    for (int q = 0; q < cw; q++) s += rowsh[r * cw + q];
+    stg(t.rowpart + (int64_t)tl.strip * t.n + tl.row(r), s);
+  }
+  for (int c = threadIdx.x; c < kChunk * cw; c += kThreads) {
+    const int q = c / kChunk, cc = c - q * kChunk;
+    double s = 0.0;
+    for (int w = q; w < kWaves; w += cw) s += colsh[w][cc];
+    const int64_t col = tl.c0 + c;
+    if (col < t.m) stg(t.colpart + (int64_t)tl.band * t.m + col, s);
   }
 }
 
@@ -226,43 +264,53 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     double rn = 0.0;
     if (i < t.n) {
       double s = 0.0;
-      for (int q = 0; q < t.ntc; q++) s += t.rowpart[(int64_t)q * t.n + i];
+      for (int q = 0; q < t.ntc; q++) s += ldg(t.rowpart + (int64_t)q * t.n + i);
       const float ri = (float)(s / (double)t.m);
-      const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, t.R[i]));
-      t.R[i] = R;
-      t.ainv[i] = 1.0 / sqrt((double)R);
+      const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, ldg(t.R + i)));
+      stg(t.R + i, R);
+      stg(t.ainv + i, 1.0 / sqrt((double)R));
       rn = (double)R;
     }
     const double tot = block_sum(rn, sh);
-    if (threadIdx.x == 0) t.rsum[it.tile] = tot;
+    if (threadIdx.x == 0) stg(t.rsum + it.tile, tot);
   } else {
     const int64_t j = (int64_t)(it.tile - t.nfr) * kFold + threadIdx.x;
     if (j < t.m) {
       double s = 0.0;
-      for (int b = 0; b < t.ntr; b++) s += t.colpart[(int64_t)b * t.m + j];
+      for (int b = 0; b < t.ntr; b++) s += ldg(t.colpart + (int64_t)b * t.m + j);
       const float cj = (float)(s / (double)t.n);
-      t.C[j] = fmaf(k.a2, cj, __fmul_rn(k.b2, t.C[j]));
+      stg(t.C + j, fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j))));
     }
   }
 }
 
-// Column factors of the rank-one reconstruction for one tile: q = max(mean R, eps) and
-// c'_j = C_j / q exactly as the oracle rounds them, and b_j = 1/sqrt(c'_j) in double,
-// so that 1/D_ij = min(b_j / sqrt(R_i), 1/sqrt(eps)) (Eq. 1 reconstruction, Alg. 1 clamps).
-__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, float eps) {
-  double sr = 0.0;
-  for (int c = 0; c < t.nfr; c++) sr += t.rsum[c];
-  return max_nan((float)(sr / (double)t.n), eps);
+// Column factors of the rank-one reconstruction: q = max(mean R, eps) and c'_j = C_j / q
+// rounded as the oracle rounds them; b_j = 1/sqrt(c'_j) in double, so that
+// 1/D_ij = min(b_j / sqrt(R_i), 1/sqrt(eps)) (Eq. 1 reconstruction with the Alg. 1 clamps).
+// fixed-order work-group sum of p[0..n): thread j sums p[j], p[j + 256], ..., then a tree;
+// every thread of the work-group must call it
+__device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh) {
+  double s = 0.0;
+  for (int64_t c = threadIdx.x; c < n; c += kThreads) s += ldg(p + c);
+  return block_sum(s, sh);
 }
-__device__ __forceinline__ void column_factors(const DevTensor &t, const Tile &tl, float q, double (&bd)[kMaxCw][8]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int qq = 0; qq < kMaxCw; qq++)
-#pragma unroll
-    for (int e = 0; e < 8; e++) {
-      const int64_t col = tl.c0 + qq * kChunk + lane * 8 + e;
-      bd[qq][e] = (qq < t.cw && col < t.m) ? 1.0 / sqrt((double)(t.C[col] / q)) : 0.0;
-    }
+// q = max(mean R, eps) for a factored tensor (the clamp of the reconstruction)
+__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, float eps, double *sh) {
+  return max_nan((float)(wg_sum(t.rsum, t.nfr, sh) / (double)t.n), eps);
+}
+__device__ __forceinline__ double col_factor(const DevTensor &t, int64_t col, float q) {
+  return 1.0 / sqrt((double)(ldg(t.C + col) / q));
+}
+
+// 8 momentum values at a 32-byte aligned position
+__device__ __forceinline__ void load_m8(const float *p, float *o) {
+  const float4 a = ldg(reinterpret_cast<const float4 *>(p));
+  const float4 b = ldg(reinterpret_cast<const float4 *>(p + 4));
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+__device__ __forceinline__ void store_m8(float *p, const float *v) {
+  stg(reinterpret_cast<float4 *>(p), make_float4(v[0], v[1], v[2], v[3]));
+  stg(reinterpret_cast<float4 *>(p + 4), make_float4(v[4], v[5], v[6], v[7]));
 }
 
 // --------------------------------------------------------------------------------------------
@@ -270,102 +318,274 @@ __device__ __forceinline__ void column_factors(const DevTensor &t, const Tile &t
 // double from the unrounded U_hat; it differs from the oracle's sum of rounded U_hat by
 // about 1e-8 / sqrt(N) relative, so the clip factor rounds to the same float.
 // --------------------------------------------------------------------------------------------
+__device__ __forceinline__ double p2_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float q) {
+  const WaveMap wm(t, tl);
+  const int64_t m = t.m, ld = t.ld, col = wm.col;
+  const bool mom = t.momentum != 0;
+  const double sd = (double)(mom ? k.s_m : k.s_0);
+  const double capd = sd / (double)sqrtf(k.eps);   // s / D at the floor, with the oracle's D
+  double acc = 0.0;
+  if (col >= m) return 0.0;
+  if (t.vec) {
+    double bd[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) bd[e] = col_factor(t, col + e, q);
+    for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
+      const bool two = lr + wm.rpi < tl.nr;
+      const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + wm.rpi) : i;
+      const uint4 ga = ldg(reinterpret_cast<const uint4 *>(t.g + i * ld + col));
+      const uint4 gb = ldg(reinterpret_cast<const uint4 *>(t.g + i2 * ld + col));
+      float ma[8], mb[8];
+      if (mom) {
+        load_m8(t.M + i * m + col, ma);
+        load_m8(t.M + i2 * m + col, mb);
+      }
+      const double aa = sd * ldg(t.ainv + i), ab = sd * ldg(t.ainv + i2);
+      float xa[8], xb[8];
+      unpack8(ga, xa);
+      unpack8(gb, xb);
+      if (mom) {
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+          xa[e] = fmaf(k.a1, xa[e], __fmul_rn(k.b1, ma[e]));
+          xb[e] = fmaf(k.a1, xb[e], __fmul_rn(k.b1, mb[e]));
+        }
+      }
+      double sa = 0.0, sb = 0.0;
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        const double ua = (double)xa[e] * fmin(aa * bd[e], capd);
+        const double ub = (double)xb[e] * fmin(ab * bd[e], capd);
+        sa = fma(ua, ua, sa);
+        sb = fma(ub, ub, sb);
+      }
+      acc += sa;
+      if (two) acc += sb;
+    }
+  } else {
+    for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    const int64_t i = tl.row(lr);
+      const double alpha = sd * ldg(t.ainv + i);
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        if (col + e >= m) continue;
+        float x = bf_one(ldg(t.g + i * ld + col + e));
+        if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
+        const double u = (double)x * fmin(alpha * col_factor(t, col + e, q), capd);
+        acc = fma(u, u, acc);
+      }
+    }
+  }
+  return acc;
+}
+
+__device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, const StepConsts &k) {
+  // exact second moment (router tier, vectors): the oracle's operation order exactly
+  const WaveMap wm(t, tl);
+  const int64_t m = t.m, ld = t.ld, col = wm.col;
+  const bool mom = t.momentum != 0;
+  double acc = 0.0;
+  for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    const int64_t i = tl.row(lr);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      if (col + e >= m) continue;
+      const int64_t sidx = i * m + col + e;
+      const float g = bf_one(ldg(t.g + i * ld + col + e));
+      const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
+      const float dd = sqrtf(max_nan(vn, k.eps));
+      const float num = mom ? __fmul_rn(k.s_m, fmaf(k.a1, g, __fmul_rn(k.b1, ldg(t.M + sidx)))) : __fmul_rn(k.s_0, g);
+      const float u = num / dd;
+      acc += (double)u * (double)u;
+    }
+  }
+  return acc;
+}
+
 __global__ __launch_bounds__(kThreads) void p2_kernel(const DevTensor *__restrict__ TT,
                                                       const Item *__restrict__ items, StepConsts k) {
   __shared__ double sh[kThreads];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   const Tile tl = tile_of(t, it.tile);
-  const int64_t m = t.m, ld = t.ld;
-  const int cw = t.cw;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const bool mom = t.momentum != 0;
-  double acc = 0.0;
-
+  double acc;
   if (t.kind == kFactored) {
-    const float q = mean_r_clamped(t, k.eps);
-    double bd[kMaxCw][8];
-    column_factors(t, tl, q, bd);
-    const double sd = (double)(mom ? k.s_m : k.s_0);
-    const double capd = sd / (double)sqrtf(k.eps);   // s / D at the floor, with the oracle's D
-    for (int64_t i = tl.r0 + wave; i < tl.r1; i += kWaves) {
-      const double alpha = sd * t.ainv[i];
-      const uint16_t *grow = t.g + i * ld;
-      const float *mrow = mom ? t.M + i * m : nullptr;
-#pragma unroll
-      for (int q = 0; q < kMaxCw; q++) {
-        if (q >= cw) continue;
-        const int64_t col = tl.c0 + q * kChunk + lane * 8;
-        if (t.vec) {
-          if (col >= m) continue;
-          float x[8];
-          unpack8(*reinterpret_cast<const uint4 *>(grow + col), x);
-          if (mom) {
-            const float4 m0 = *reinterpret_cast<const float4 *>(mrow + col);
-            const float4 m1 = *reinterpret_cast<const float4 *>(mrow + col + 4);
-            const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-#pragma unroll
-            for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
-          }
-#pragma unroll
-          for (int e = 0; e < 8; e++) {
-            const double u = (double)x[e] * fmin(alpha * bd[q][e], capd);
-            acc = fma(u, u, acc);
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; e++) {
-            if (col + e >= m) continue;
-            float x = bf_one(grow[col + e]);
-            if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, mrow[col + e]));
-            const double u = (double)x * fmin(alpha * bd[q][e], capd);
-            acc = fma(u, u, acc);
-          }
-        }
-      }
-    }
+    const float q = mean_r_clamped(t, k.eps, sh);
+    acc = p2_factored(t, tl, k, q);
   } else {
-    // exact second moment (router tier, vectors): the oracle's operation order exactly
-    for (int64_t i = tl.r0 + wave; i < tl.r1; i += kWaves) {
-      const uint16_t *grow = t.g + i * ld;
-#pragma unroll
-      for (int q = 0; q < kMaxCw; q++) {
-        if (q >= cw) continue;
-        const int64_t col = tl.c0 + q * kChunk + lane * 8;
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-          if (col + e >= m) continue;
-          const int64_t sidx = i * m + col + e;
-          const float g = bf_one(grow[col + e]);
-          const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, t.V[sidx]));
-          const float dd = sqrtf(max_nan(vn, k.eps));
-          const float num = mom ? __fmul_rn(k.s_m, fmaf(k.a1, g, __fmul_rn(k.b1, t.M[sidx]))) : __fmul_rn(k.s_0, g);
-          const float u = num / dd;
-          acc += (double)u * (double)u;
-        }
-      }
-    }
+    acc = p2_exact(t, tl, k);
   }
   const double tot = block_sum(acc, sh);
-  if (threadIdx.x == 0) t.ssum[it.tile] = tot;
+  if (threadIdx.x == 0) stg(t.ssum + it.tile, tot);
 }
 
 // The oracle's float sequence for one factored element (Alg. 1 with the eps clamps):
 // D = sqrt(max(R_i * c'_j, eps)), U = ((s * x) / D) * k, y = (w - lr U) + xi.
-__device__ __attribute__((noinline)) float exact_factored_y(float x, float w, float Ri, float cpj, float s, float kc,
-                                                            float eps, float lr, float dith) {
+__device__ __forceinline__ float exact_factored_y(float x, float w, float Ri, float cpj, float s, float kc,
+                                                  float eps, float lr, float dith) {
   const float vh = __fmul_rn(Ri, cpj);
   const float dd = sqrtf(max_nan(vh, eps));
   const float U = __fmul_rn(__fmul_rn(s, x) / dd, kc);
   return fmaf(dith, fabsf(w), fmaf(-lr, U, w));
 }
 
-// True when y may round differently from the oracle's value: the fast update g*F differs
+// True when y may round differently from the oracle's value: the fast update x*F differs
 // from the oracle's lr*U by < 2^-19 relative, and each of x and y carries one rounding.
-__device__ __forceinline__ bool near_boundary(float y, float gF, float w) {
+__device__ __forceinline__ bool near_boundary(float y, float xF, float w) {
   const float mid = __uint_as_float((__float_as_uint(y) & 0xFFFF0000u) | 0x8000u);
-  const float bound = fmaf(fabsf(gF), 0x1p-18f + 0x1p-21f, fabsf(w) * 0x1p-21f);
+  const float bound = fmaf(fabsf(xF), 0x1p-18f + 0x1p-21f, fabsf(w) * 0x1p-21f);
   return fabsf(y - mid) <= bound;
+}
+
+// clip factor k = 1 / max(1, RMS(U_hat) / d), NaN-propagating, rounded once as the oracle
+__device__ __forceinline__ float clip_factor(const DevTensor &t, float d, double *sh) {
+  const double S = wg_sum(t.ssum, (int64_t)t.ntr * t.ntc, sh);
+  const double ratio = sqrt(S / (double)(t.n * t.m)) / (double)d;
+  const double den = (ratio != ratio) ? ratio : (ratio < 1.0 ? 1.0 : ratio);
+  return (float)(1.0 / den);
+}
+
+struct P3Scalars {
+  float q, s, kc, cap3, eps, lr;
+  double lsk;
+};
+
+// one row segment of 8 elements (vector path): momentum, update, dither, bf16 store.
+// The fast path forms 1/D from per-row and per-column factors; the few elements whose
+// result might round to the other bf16 neighbour take the oracle's exact sequence.
+__device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k, const P3Scalars &c,
+                                        const Dither &dz, int64_t i, int64_t col, const float *bf, uint4 gw,
+                                        uint4 ww, const float *mv) {
+  const bool mom = t.momentum != 0;
+  float x[8], w[8];
+  unpack8(gw, x);
+  unpack8(ww, w);
+  if (mom) {
+#pragma unroll
+    for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
+    store_m8(t.M + i * t.m + col, x);
+  }
+  const float alpha = (float)(c.lsk * ldg(t.ainv + i));
+  const uint64_t p0 = ((uint64_t)i * (uint64_t)t.m + (uint64_t)col) >> 1;   // m and col are even here
+  float y[8], dith[8];
+  bool any = false;
+#pragma unroll
+  for (int e2 = 0; e2 < 4; e2++) {
+    const uint32_t h = dz.pair(p0 + e2);
+    dith[2 * e2] = dither_lo(h);
+    dith[2 * e2 + 1] = dither_hi(h);
+  }
+#pragma unroll
+  for (int e = 0; e < 8; e++) {
+    const float F = fminf(alpha * bf[e], c.cap3);
+    y[e] = fmaf(dith[e], fabsf(w[e]), fmaf(-x[e], F, w[e]));
+    any |= near_boundary(y[e], x[e] * F, w[e]);
+  }
+  if (any) {
+    const float Ri = ldg(t.R + i);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      const float F = fminf(alpha * bf[e], c.cap3);
+      if (near_boundary(y[e], x[e] * F, w[e]))
+        y[e] = exact_factored_y(x[e], w[e], Ri, ldg(t.C + col + e) / c.q, c.s, c.kc, c.eps, c.lr, dith[e]);
+    }
+  }
+  stg(reinterpret_cast<uint4 *>(t.w + i * t.ld + col),
+      make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                 pack_bf16x2(y[6], y[7])));
+}
+
+__device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float kc,
+                                            float q, const Dither &dz) {
+  const WaveMap wm(t, tl);
+  const int64_t m = t.m, ld = t.ld, col = wm.col;
+  const bool mom = t.momentum != 0;
+  if (col >= m) return;
+  P3Scalars c;
+  c.q = q;
+  c.s = mom ? k.s_m : k.s_0;
+  c.kc = kc;
+  c.eps = k.eps;
+  c.lr = k.lr;
+  c.lsk = (double)k.lr * (double)c.s * (double)kc;   // lr * s * k
+  c.cap3 = (float)(c.lsk / (double)sqrtf(k.eps));
+  if (t.vec) {
+    float bf[8];
+#pragma unroll
+    for (int e = 0; e < 8; e++) bf[e] = (float)col_factor(t, col + e, c.q);
+    for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
+      const bool two = lr + wm.rpi < tl.nr;
+      const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + wm.rpi) : i;
+      const uint4 ga = ldg(reinterpret_cast<const uint4 *>(t.g + i * ld + col));
+      const uint4 wa = ldg(reinterpret_cast<const uint4 *>(t.w + i * ld + col));
+      const uint4 gb = ldg(reinterpret_cast<const uint4 *>(t.g + i2 * ld + col));
+      const uint4 wb = ldg(reinterpret_cast<const uint4 *>(t.w + i2 * ld + col));
+      float ma[8], mb[8];
+      if (mom) {
+        load_m8(t.M + i * m + col, ma);
+        load_m8(t.M + i2 * m + col, mb);
+      }
+      p3_row8(t, k, c, dz, i, col, bf, ga, wa, ma);
+      if (two) p3_row8(t, k, c, dz, i2, col, bf, gb, wb, mb);
+    }
+  } else {
+    for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    const int64_t i = tl.row(lr);
+      const float alpha = (float)(c.lsk * ldg(t.ainv + i));
+      const uint64_t rowidx = (uint64_t)i * (uint64_t)m;
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        if (col + e >= m) continue;
+        float x = bf_one(ldg(t.g + i * ld + col + e));
+        const float w = bf_one(ldg(t.w + i * ld + col + e));
+        if (mom) {
+          x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
+          stg(t.M + i * m + col + e, x);
+        }
+        const uint64_t idx = rowidx + (uint64_t)(col + e);
+        const float dith = dither_of(dz.pair(idx >> 1), idx);
+        const float F = fminf(alpha * (float)col_factor(t, col + e, c.q), c.cap3);
+        float y = fmaf(dith, fabsf(w), fmaf(-x, F, w));
+        if (near_boundary(y, x * F, w))
+          y = exact_factored_y(x, w, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith);
+        stg(t.w + i * ld + col + e, to_bf16(y));
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, const StepConsts &k, float kc,
+                                         const Dither &dz) {
+  // exact second moment: the oracle's operation order exactly
+  const WaveMap wm(t, tl);
+  const int64_t m = t.m, ld = t.ld, col = wm.col;
+  const bool mom = t.momentum != 0;
+  for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    const int64_t i = tl.row(lr);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      if (col + e >= m) continue;
+      const int64_t sidx = i * m + col + e;
+      const float g = bf_one(ldg(t.g + i * ld + col + e));
+      const float w = bf_one(ldg(t.w + i * ld + col + e));
+      const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
+      stg(t.V + sidx, vn);
+      const float dd = sqrtf(max_nan(vn, k.eps));
+      float num;
+      if (mom) {
+        const float mn = fmaf(k.a1, g, __fmul_rn(k.b1, ldg(t.M + sidx)));
+        stg(t.M + sidx, mn);
+        num = __fmul_rn(k.s_m, mn);
+      } else {
+        num = __fmul_rn(k.s_0, g);
+      }
+      const float U = __fmul_rn(num / dd, kc);
+      const float x = fmaf(-k.lr, U, w);
+      const uint64_t idx = (uint64_t)sidx;
+      const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), fabsf(w), x);
+      stg(t.w + i * ld + col + e, to_bf16(y));
+    }
+  }
 }
 
 // --------------------------------------------------------------------------------------------
@@ -375,133 +595,15 @@ __global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restric
                                                       const Item *__restrict__ items, StepConsts k) {
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
+  __shared__ double sh[kThreads];
   const Tile tl = tile_of(t, it.tile);
-  const int64_t m = t.m, ld = t.ld;
-  const int cw = t.cw;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const bool mom = t.momentum != 0;
-
-  // clip factor k = 1 / max(1, RMS(U_hat) / d), NaN-propagating, rounded once as the oracle
-  double S = 0.0;
-  const int ntiles = t.ntr * t.ntc;
-  for (int c = 0; c < ntiles; c++) S += t.ssum[c];
-  const double ratio = sqrt(S / (double)(t.n * m)) / (double)k.d;
-  const double den = (ratio != ratio) ? ratio : (ratio < 1.0 ? 1.0 : ratio);
-  const float kc = (float)(1.0 / den);
+  const float kc = clip_factor(t, k.d, sh);
   const Dither dz(k.seed, k.step, t.tensor_id);
-
   if (t.kind == kFactored) {
-    const float q = mean_r_clamped(t, k.eps);
-    float bf[kMaxCw][8];
-    {
-      double bd[kMaxCw][8];
-      column_factors(t, tl, q, bd);
-#pragma unroll
-      for (int qq = 0; qq < kMaxCw; qq++)
-#pragma unroll
-        for (int e = 0; e < 8; e++) bf[qq][e] = (float)bd[qq][e];
-    }
-    const float s = mom ? k.s_m : k.s_0;
-    const double lsk = (double)k.lr * (double)s * (double)kc;   // lr * s * k
-    const float cap3 = (float)(lsk / (double)sqrtf(k.eps));
-    for (int64_t i = tl.r0 + wave; i < tl.r1; i += kWaves) {
-      const float alpha = (float)(lsk * t.ainv[i]);
-      const float Ri = t.R[i];
-      const uint16_t *grow = t.g + i * ld;
-      uint16_t *wrow = t.w + i * ld;
-      float *mrow = mom ? t.M + i * m : nullptr;
-      const uint64_t rowidx = (uint64_t)i * (uint64_t)m;
-#pragma unroll
-      for (int qc = 0; qc < kMaxCw; qc++) {
-        if (qc >= cw) continue;
-        const int64_t col = tl.c0 + qc * kChunk + lane * 8;
-        if (t.vec) {
-          if (col >= m) continue;
-          float x[8], w[8];
-          unpack8(*reinterpret_cast<const uint4 *>(grow + col), x);
-          unpack8(*reinterpret_cast<const uint4 *>(wrow + col), w);
-          if (mom) {
-            const float4 m0 = *reinterpret_cast<const float4 *>(mrow + col);
-            const float4 m1 = *reinterpret_cast<const float4 *>(mrow + col + 4);
-            const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-#pragma unroll
-            for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
-            *reinterpret_cast<float4 *>(mrow + col) = make_float4(x[0], x[1], x[2], x[3]);
-            *reinterpret_cast<float4 *>(mrow + col + 4) = make_float4(x[4], x[5], x[6], x[7]);
-          }
-          const uint64_t p0 = (rowidx + (uint64_t)col) >> 1;   // m and col are even here
-          uint32_t out[4];
-#pragma unroll
-          for (int e2 = 0; e2 < 4; e2++) {
-            const uint32_t h = dz.pair(p0 + e2);
-            float y[2];
-#pragma unroll
-            for (int h2 = 0; h2 < 2; h2++) {
-              const int e = 2 * e2 + h2;
-              const float dith = h2 ? dither_hi(h) : dither_lo(h);
-              const float F = fminf(alpha * bf[qc][e], cap3);
-              const float yf = fmaf(dith, fabsf(w[e]), fmaf(-x[e], F, w[e]));
-              y[h2] = yf;
-              if (near_boundary(yf, x[e] * F, w[e]))
-                y[h2] = exact_factored_y(x[e], w[e], Ri, t.C[col + e] / q, s, kc, k.eps, k.lr, dith);
-            }
-            out[e2] = pack_bf16x2(y[0], y[1]);
-          }
-          *reinterpret_cast<uint4 *>(wrow + col) = make_uint4(out[0], out[1], out[2], out[3]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; e++) {
-            if (col + e >= m) continue;
-            float x = bf_one(grow[col + e]);
-            const float w = bf_one(wrow[col + e]);
-            if (mom) {
-              x = fmaf(k.a1, x, __fmul_rn(k.b1, mrow[col + e]));
-              mrow[col + e] = x;
-            }
-            const uint64_t idx = rowidx + (uint64_t)(col + e);
-            const float dith = dither_of(dz.pair(idx >> 1), idx);
-            const float F = fminf(alpha * bf[qc][e], cap3);
-            float y = fmaf(dith, fabsf(w), fmaf(-x, F, w));
-            if (near_boundary(y, x * F, w)) y = exact_factored_y(x, w, Ri, t.C[col + e] / q, s, kc, k.eps, k.lr, dith);
-            wrow[col + e] = to_bf16(y);
-          }
-        }
-      }
-    }
+    const float q = mean_r_clamped(t, k.eps, sh);
+    p3_factored(t, tl, k, kc, q, dz);
   } else {
-    // exact second moment: the oracle's operation order exactly
-    for (int64_t i = tl.r0 + wave; i < tl.r1; i += kWaves) {
-      const uint16_t *grow = t.g + i * ld;
-      uint16_t *wrow = t.w + i * ld;
-#pragma unroll
-      for (int q = 0; q < kMaxCw; q++) {
-        if (q >= cw) continue;
-        const int64_t col = tl.c0 + q * kChunk + lane * 8;
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-          if (col + e >= m) continue;
-          const int64_t sidx = i * m + col + e;
-          const float g = bf_one(grow[col + e]);
-          const float w = bf_one(wrow[col + e]);
-          const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, t.V[sidx]));
-          t.V[sidx] = vn;
-          const float dd = sqrtf(max_nan(vn, k.eps));
-          float num;
-          if (mom) {
-            const float mn = fmaf(k.a1, g, __fmul_rn(k.b1, t.M[sidx]));
-            t.M[sidx] = mn;
-            num = __fmul_rn(k.s_m, mn);
-          } else {
-            num = __fmul_rn(k.s_0, g);
-          }
-          const float U = __fmul_rn(num / dd, kc);
-          const float x = fmaf(-k.lr, U, w);
-          const uint64_t idx = (uint64_t)sidx;
-          const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), fabsf(w), x);
-          wrow[col + e] = to_bf16(y);
-        }
-      }
-    }
+    p3_exact(t, tl, k, kc, dz);
   }
 }
 

@@ -54,8 +54,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.off_c = st; st = align_up(st + (size_t)tp.m * 4);
     }
 
-    // tile grid: tr rows x (512 * cw) columns, about kTileElems elements
-    tp.cw = (int32_t)std::min<int64_t>(kMaxCw, ceil_div(tp.m, kChunk));
+    // tile grid: tr rows x (512 * cw) columns, about kTileElems elements; cw in {1, 2, 4}
+    // so that the four waves of a work-group map onto (chunk, row) pairs statically
+    tp.cw = tp.m > 2 * kChunk ? 4 : (tp.m > kChunk ? 2 : 1);
     const int64_t tc = (int64_t)kChunk * tp.cw;
     tp.tr = std::max<int64_t>(1, kTileElems / tc);
     const int64_t ntc = ceil_div(tp.m, tc), ntr = ceil_div(tp.n, tp.tr);

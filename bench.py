@@ -107,6 +107,9 @@ def main() -> int:
     ap.add_argument("--workload", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run three plain 1 GiB device-to-device copies (read 1 GiB, write 1 GiB "
+                         "each), whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -123,6 +126,15 @@ def main() -> int:
         return 1
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
+    if args.calibrate_copy:
+        src = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] calibration copies done (3 x 1 GiB)")
     wl = W.get(args.workload)
     log(f"[bench] workload {wl.name}: {len(wl.specs)} tensors, {wl.numel:,} params; allocating")
     Wt = [W.init_weight(s, wl, dev) for s in wl.specs]

@@ -47,6 +47,8 @@ enum {
 
 enum { SKEW_TIER_BACKBONE = 0, SKEW_TIER_EXPERT = 1, SKEW_TIER_ROUTER = 2 };
 
+enum { SKEW_FLAG_EXACT_CLIP = 1 };
+
 /* One parameter tensor (Sec. 3 "The tiers": the policy assigns state by parameter role).
  *   tier      SKEW_TIER_*.
  *   ndim      2 = matrix (row-major, `rows` x `cols`, row stride `ld` elements);
@@ -86,7 +88,9 @@ typedef struct skew_tensor_desc {
  *   eps             > 0: floor of the second moment, and of mean(R) in the
  *                   factored reconstruction.
  *   clip_threshold  d > 0 (may be +inf: no clipping): U <- U / max(1, RMS(U)/d).
- *   flags           must be 0.
+ *   flags           0, or SKEW_FLAG_EXACT_CLIP: always recompute the sum of squares behind
+ *                   the clip factor with the reference float sequence (by default it is
+ *                   recomputed only when a faster estimate cannot decide its rounding).
  *   step            t >= 1, the caller's step counter (the library keeps none).
  *   seed            dither seed; with (step, tensor_id, element index) it fixes
  *                   every dither value, so results are bit-reproducible. */

@@ -12,15 +12,15 @@
 using namespace skew;
 
 namespace {
-constexpr int kLaunches = 4;
-const char *const kLaunchNames[kLaunches] = {"p1_rowcol_sumsq", "fold_rc_ema", "p2_update_sumsq",
-                                             "p3_apply_dither"};
+constexpr int kLaunches = 7;
+const char *const kLaunchNames[kLaunches] = {"p1_rowcol_sumsq", "fold_rc_ema", "p2_update_sumsq", "clip_factor",
+                                             "p2_exact_recheck", "clip_factor_recheck", "p3_apply_dither"};
 }  // namespace
 
 struct skew_ctx {
   Plan plan;
   DevTensor *d_table = nullptr;
-  Item *d_p1 = nullptr, *d_fold = nullptr, *d_p2 = nullptr, *d_p3 = nullptr;
+  Item *d_p1 = nullptr, *d_fold = nullptr, *d_p2 = nullptr, *d_p3 = nullptr, *d_clip = nullptr;
   // diagnostics: events [step][kLaunches + 1]
   std::vector<hipEvent_t> ev;
   int ev_steps = 0, ev_used = 0;
@@ -51,12 +51,13 @@ StepConsts make_consts(const skew_hparams &hp) {
   k.s_0 = (float)std::sqrt(bc2);
   k.step = hp.step;
   k.seed = hp.seed;
+  k.flags = hp.flags;
   return k;
 }
 
 bool hparams_ok(const skew_hparams *hp) {
   if (hp == nullptr) return false;
-  if (hp->flags != 0 || hp->step < 1) return false;
+  if ((hp->flags & ~SKEW_FLAG_EXACT_CLIP) != 0 || hp->step < 1) return false;
   if (!std::isfinite(hp->lr)) return false;
   if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f)) return false;
   if (!(hp->beta2 >= 0.0f && hp->beta2 < 1.0f)) return false;
@@ -123,6 +124,8 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.R = d[i].r;
     x.C = d[i].c;
     x.ssum = reinterpret_cast<double *>(ws + tp.off_ssum);
+    x.qsum = reinterpret_cast<double *>(ws + tp.off_qsum);
+    x.sc = reinterpret_cast<TensorScalars *>(ws + tp.off_sc);
     if (tp.kind == kFactored) {
       x.rowpart = reinterpret_cast<double *>(ws + tp.off_rowpart);
       x.colpart = reinterpret_cast<double *>(ws + tp.off_colpart);
@@ -144,11 +147,12 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.tensor_id = d[i].tensor_id;
   }
   std::vector<Item> items;
-  items.reserve(p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + 1);
+  items.reserve(p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
   items.insert(items.end(), p.p1.begin(), p.p1.end());
   items.insert(items.end(), p.fold.begin(), p.fold.end());
   items.insert(items.end(), p.p2.begin(), p.p2.end());
   items.insert(items.end(), p.p3.begin(), p.p3.end());
+  items.insert(items.end(), p.clip.begin(), p.clip.end());
   if (items.empty()) items.push_back({0, 0});
 
   skew_ctx *c = new (std::nothrow) skew_ctx;
@@ -159,6 +163,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   c->d_fold = c->d_p1 + p.p1.size();
   c->d_p2 = c->d_fold + p.fold.size();
   c->d_p3 = c->d_p2 + p.p2.size();
+  c->d_clip = c->d_p3 + p.p3.size();
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipSuccess;
@@ -191,8 +196,14 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (e == 0 && ev) e = (int)hipEventRecord(ev[2], s);
   if (e == 0) e = launch_p2(ctx->d_table, ctx->d_p2, (int64_t)p.p2.size(), k, stream);
   if (e == 0 && ev) e = (int)hipEventRecord(ev[3], s);
-  if (e == 0) e = launch_p3(ctx->d_table, ctx->d_p3, (int64_t)p.p3.size(), k, stream);
+  if (e == 0) e = launch_clip(ctx->d_table, ctx->d_clip, (int64_t)p.clip.size(), k, 0, stream);
   if (e == 0 && ev) e = (int)hipEventRecord(ev[4], s);
+  if (e == 0) e = launch_p2_exact(ctx->d_table, ctx->d_p2, (int64_t)p.p2.size(), k, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[5], s);
+  if (e == 0) e = launch_clip(ctx->d_table, ctx->d_clip, (int64_t)p.clip.size(), k, 1, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[6], s);
+  if (e == 0) e = launch_p3(ctx->d_table, ctx->d_p3, (int64_t)p.p3.size(), k, stream);
+  if (e == 0 && ev) e = (int)hipEventRecord(ev[7], s);
   return e == 0 ? SKEW_OK : SKEW_EHIP;
 }
 

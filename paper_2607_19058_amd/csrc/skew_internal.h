@@ -18,6 +18,14 @@ constexpr int kFold = 256;              // rows (or columns) folded by one work-
 constexpr int64_t kTileElems = 1 << 19; // target elements per tile: 1 MiB of bf16 gradient
 constexpr size_t kAlign = 256;
 
+// Per-tensor scalars of one step, written by the clip stage and read by the update.
+struct TensorScalars {
+  float k;            // clip factor 1 / max(1, RMS(U_hat) / d), rounded as the oracle rounds it
+  float q;            // max(mean R, eps) (factored tensors)
+  int32_t ambiguous;  // 1: the approximate sum left k's rounding undecided; the exact pass decides
+  int32_t pad;
+};
+
 // Device-resident description of one tensor, its state and its partial sums.
 struct DevTensor {
   uint16_t *w;
@@ -28,6 +36,8 @@ struct DevTensor {
   double *ainv;           // [n]        1/sqrt(R_i) after the step's EMA
   double *rsum;           // [nfr]      sums of R_i over each fold chunk of rows
   double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
+  double *qsum;           // [ntr*ntc]  per-tile sums of U_hat^4 over the approximated elements
+  TensorScalars *sc;      // this step's clip factor and reconstruction clamp
   int64_t n, m, ld;       // rows, columns, row stride (elements)
   int64_t tr;             // rows per tile
   int32_t cw;             // 512-column chunks per tile (1, 2 or 4)
@@ -47,7 +57,7 @@ struct Item {
 // Per-step scalars (Alg. 1), computed on the host in double and rounded once.
 struct StepConsts {
   float b1, a1, b2, a2, eps, lr, d, s_m, s_0;
-  int32_t pad;
+  int32_t flags;   // SKEW_FLAG_*
   int64_t step;
   uint64_t seed;
 };
@@ -63,12 +73,12 @@ struct TensorPlan {
   size_t off_m = SIZE_MAX, off_v = SIZE_MAX, off_r = SIZE_MAX, off_c = SIZE_MAX;
   // workspace offsets in bytes
   size_t off_rowpart = SIZE_MAX, off_colpart = SIZE_MAX, off_ainv = SIZE_MAX, off_rsum = SIZE_MAX,
-         off_ssum = SIZE_MAX;
+         off_ssum = SIZE_MAX, off_qsum = SIZE_MAX, off_sc = SIZE_MAX;
 };
 
 struct Plan {
   std::vector<TensorPlan> t;
-  std::vector<Item> p1, fold, p2, p3;
+  std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
   size_t state_bytes = 0;
   size_t ws_bytes = 0;
   size_t off_table = 0, off_items = 0;   // workspace offsets of the device table and item lists
@@ -84,5 +94,7 @@ int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream
 int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int exact, void *stream);
+int launch_p2_exact(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 
 }  // namespace skew

@@ -314,22 +314,50 @@ __device__ __forceinline__ void store_m8(float *p, const float *v) {
 }
 
 // --------------------------------------------------------------------------------------------
-// p2: per-tile sum of squares of the unclipped update U_hat (Alg. 1, before clipping), in
-// double from the unrounded U_hat; it differs from the oracle's sum of rounded U_hat by
-// about 1e-8 / sqrt(N) relative, so the clip factor rounds to the same float.
+// p2: per-tile sum of squares of the unclipped update U_hat (Alg. 1, before clipping).
+//
+// The clip factor must round to the oracle's float, so the sum must match the oracle's
+// sum of its rounded U_hat to ~1e-13. Roundings that repeat a pattern are replicated
+// exactly: s*x (a fixed s times 8-bit bf16 mantissas) and, on the floor, the division
+// by the constant D = sqrt(eps) (Markstein's correctly rounded division with the
+// correctly rounded reciprocal). Above the floor the oracle's three roundings (of R_i c'_j,
+// the square root and the quotient) vary freely from element to element, so U_hat is
+// taken unrounded in double, and the sum of U_hat^4 over those elements gives the
+// spread of the difference. The clip stage decides k from this; when the bound leaves
+// k's rounding open, an exact pass (p2_exact) recomputes the tensor's sum.
 // --------------------------------------------------------------------------------------------
-__device__ __forceinline__ double p2_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float q) {
+struct SumPair {
+  double s, q4;
+};
+
+__device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float q) {
   const WaveMap wm(t, tl);
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
-  const double sd = (double)(mom ? k.s_m : k.s_0);
-  const double capd = sd / (double)sqrtf(k.eps);   // s / D at the floor, with the oracle's D
-  double acc = 0.0;
-  if (col >= m) return 0.0;
-  if (t.vec) {
-    double bd[8];
+  const float s = mom ? k.s_m : k.s_0;
+  const float deps = sqrtf(k.eps);                    // the oracle's D on the floor
+  const float reps = (float)(1.0 / (double)deps);     // correctly rounded 1/D
+  SumPair acc = {0.0, 0.0};
+  if (col >= m) return acc;
+  float cp[8];    // c'_j = C_j / q, rounded as the oracle
+  double bd[8];   // 1/sqrt(c'_j)
 #pragma unroll
-    for (int e = 0; e < 8; e++) bd[e] = col_factor(t, col + e, q);
+  for (int e = 0; e < 8; e++) {
+    cp[e] = (col + e < m) ? ldg(t.C + col + e) / q : 0.f;
+    bd[e] = 1.0 / sqrt((double)cp[e]);
+  }
+  auto elem = [&](float x, float Ri, double ai, int e, SumPair &a) {
+    const float ax = __fmul_rn(s, x);
+    const bool floored = __fmul_rn(Ri, cp[e]) < k.eps;
+    const float q0 = ax * reps;
+    const float uf = fmaf(fmaf(-q0, deps, ax), reps, q0);   // RN(ax / deps)
+    const double ud = (double)ax * (ai * bd[e]);
+    const double u = floored ? (double)uf : ud;
+    a.s = fma(u, u, a.s);
+    const double u2 = floored ? 0.0 : ud * ud;
+    a.q4 = fma(u2, u2, a.q4);
+  };
+  if (t.vec) {
     for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
       const bool two = lr + wm.rpi < tl.nr;
       const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + wm.rpi) : i;
@@ -340,7 +368,8 @@ __device__ __forceinline__ double p2_factored(const DevTensor &t, const Tile &tl
         load_m8(t.M + i * m + col, ma);
         load_m8(t.M + i2 * m + col, mb);
       }
-      const double aa = sd * ldg(t.ainv + i), ab = sd * ldg(t.ainv + i2);
+      const float Ra = ldg(t.R + i), Rb = ldg(t.R + i2);
+      const double aa = ldg(t.ainv + i), ab = ldg(t.ainv + i2);
       float xa[8], xb[8];
       unpack8(ga, xa);
       unpack8(gb, xb);
@@ -351,29 +380,59 @@ __device__ __forceinline__ double p2_factored(const DevTensor &t, const Tile &tl
           xb[e] = fmaf(k.a1, xb[e], __fmul_rn(k.b1, mb[e]));
         }
       }
-      double sa = 0.0, sb = 0.0;
+      SumPair sa = {0.0, 0.0}, sb = {0.0, 0.0};
 #pragma unroll
       for (int e = 0; e < 8; e++) {
-        const double ua = (double)xa[e] * fmin(aa * bd[e], capd);
-        const double ub = (double)xb[e] * fmin(ab * bd[e], capd);
-        sa = fma(ua, ua, sa);
-        sb = fma(ub, ub, sb);
+        elem(xa[e], Ra, aa, e, sa);
+        elem(xb[e], Rb, ab, e, sb);
       }
-      acc += sa;
-      if (two) acc += sb;
+      acc.s += sa.s;
+      acc.q4 += sa.q4;
+      if (two) {
+        acc.s += sb.s;
+        acc.q4 += sb.q4;
+      }
     }
   } else {
     for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
-    const int64_t i = tl.row(lr);
-      const double alpha = sd * ldg(t.ainv + i);
+      const int64_t i = tl.row(lr);
+      const float Ri = ldg(t.R + i);
+      const double ai = ldg(t.ainv + i);
 #pragma unroll
       for (int e = 0; e < 8; e++) {
         if (col + e >= m) continue;
         float x = bf_one(ldg(t.g + i * ld + col + e));
         if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
-        const double u = (double)x * fmin(alpha * col_factor(t, col + e, q), capd);
-        acc = fma(u, u, acc);
+        elem(x, Ri, ai, e, acc);
       }
+    }
+  }
+  return acc;
+}
+
+// The oracle's own float sequence for U_hat of a factored tensor, summed in double:
+// used when the approximate sum leaves the clip factor's rounding undecided.
+__device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Tile &tl, const StepConsts &k,
+                                                    float q) {
+  const WaveMap wm(t, tl);
+  const int64_t m = t.m, ld = t.ld, col = wm.col;
+  const bool mom = t.momentum != 0;
+  const float s = mom ? k.s_m : k.s_0;
+  double acc = 0.0;
+  if (col >= m) return 0.0;
+  float cp[8];
+#pragma unroll
+  for (int e = 0; e < 8; e++) cp[e] = (col + e < m) ? ldg(t.C + col + e) / q : 0.f;
+  for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    const int64_t i = tl.row(lr);
+    const float Ri = ldg(t.R + i);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      if (col + e >= m) continue;
+      float x = bf_one(ldg(t.g + i * ld + col + e));
+      if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
+      const float u = __fmul_rn(s, x) / sqrtf(max_nan(__fmul_rn(Ri, cp[e]), k.eps));
+      acc = fma((double)u, (double)u, acc);
     }
   }
   return acc;
@@ -408,15 +467,77 @@ __global__ __launch_bounds__(kThreads) void p2_kernel(const DevTensor *__restric
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   const Tile tl = tile_of(t, it.tile);
-  double acc;
+  SumPair acc;
   if (t.kind == kFactored) {
     const float q = mean_r_clamped(t, k.eps, sh);
     acc = p2_factored(t, tl, k, q);
   } else {
-    acc = p2_exact(t, tl, k);
+    acc.s = p2_exact(t, tl, k);   // already the oracle's own U_hat
+    acc.q4 = 0.0;
   }
-  const double tot = block_sum(acc, sh);
-  if (threadIdx.x == 0) stg(t.ssum + it.tile, tot);
+  const double s = block_sum(acc.s, sh);
+  const double q4 = block_sum(acc.q4, sh);
+  if (threadIdx.x == 0) {
+    stg(t.ssum + it.tile, s);
+    stg(t.qsum + it.tile, q4);
+  }
+}
+
+// exact re-run of p2 for the tensors the clip stage left undecided (others exit at once)
+__global__ __launch_bounds__(kThreads) void p2_exact_kernel(const DevTensor *__restrict__ TT,
+                                                            const Item *__restrict__ items, StepConsts k) {
+  __shared__ double sh[kThreads];
+  const Item it = items[blockIdx.x];
+  const DevTensor &t = TT[it.tensor];
+  if (t.kind != kFactored || ldg(&t.sc->ambiguous) == 0) return;
+  const Tile tl = tile_of(t, it.tile);
+  const float q = mean_r_clamped(t, k.eps, sh);
+  const double s = block_sum(p2_factored_exact(t, tl, k, q), sh);
+  if (threadIdx.x == 0) stg(t.ssum + it.tile, s);
+}
+
+// --------------------------------------------------------------------------------------------
+// clip stage, one work-group per tensor: k = 1 / max(1, RMS(U_hat) / d) (Sec. 3, Alg. 1),
+// NaN-propagating and rounded once to float as the oracle rounds it. With exact == 0 it
+// also records q = max(mean R, eps) and flags the tensor when the approximate sum's
+// spread (20 standard deviations, from the sum of U_hat^4) reaches a rounding boundary
+// of k or the clipping threshold; with exact == 1 it recomputes k of flagged tensors
+// from the exact sums.
+// --------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restrict__ TT,
+                                                        const Item *__restrict__ items, StepConsts k, int exact) {
+  __shared__ double sh[kThreads];
+  const Item it = items[blockIdx.x];
+  const DevTensor &t = TT[it.tensor];
+  if (exact && ldg(&t.sc->ambiguous) == 0) return;
+  const int64_t ntiles = (int64_t)t.ntr * t.ntc;
+  const double S = wg_sum(t.ssum, ntiles, sh);
+  const double Q4 = exact ? 0.0 : wg_sum(t.qsum, ntiles, sh);
+  const float q = (!exact && t.kind == kFactored) ? mean_r_clamped(t, k.eps, sh) : 0.f;
+  if (threadIdx.x != 0) return;
+  const double r = sqrt(S / (double)(t.n * t.m)) / (double)k.d;
+  const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
+  const double kd = 1.0 / den;
+  const float kf = (float)kd;
+  if (exact) {
+    stg(&t.sc->k, kf);
+    stg(&t.sc->ambiguous, 2);
+    return;
+  }
+  bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t.kind == kFactored;
+  if (S > 0.0 && r == r && r < 1e300) {
+    const double spread = 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14;   // relative, on S
+    if (fabs(r - 1.0) <= spread) amb = true;                         // at the clipping threshold
+    if (r > 1.0) {
+      const double up = (double)nextafterf(kf, 3.0e38f), dn = (double)nextafterf(kf, 0.f);
+      const double mid_hi = 0.5 * ((double)kf + up), mid_lo = 0.5 * ((double)kf + dn);
+      const double tol = 0.5 * spread * kd;
+      if (fabs(kd - mid_hi) <= tol || fabs(kd - mid_lo) <= tol) amb = true;
+    }
+  }
+  stg(&t.sc->k, kf);
+  stg(&t.sc->q, q);
+  stg(&t.sc->ambiguous, amb ? 1 : 0);
 }
 
 // The oracle's float sequence for one factored element (Alg. 1 with the eps clamps):
@@ -435,14 +556,6 @@ __device__ __forceinline__ bool near_boundary(float y, float xF, float w) {
   const float mid = __uint_as_float((__float_as_uint(y) & 0xFFFF0000u) | 0x8000u);
   const float bound = fmaf(fabsf(xF), 0x1p-18f + 0x1p-21f, fabsf(w) * 0x1p-21f);
   return fabsf(y - mid) <= bound;
-}
-
-// clip factor k = 1 / max(1, RMS(U_hat) / d), NaN-propagating, rounded once as the oracle
-__device__ __forceinline__ float clip_factor(const DevTensor &t, float d, double *sh) {
-  const double S = wg_sum(t.ssum, (int64_t)t.ntr * t.ntc, sh);
-  const double ratio = sqrt(S / (double)(t.n * t.m)) / (double)d;
-  const double den = (ratio != ratio) ? ratio : (ratio < 1.0 ? 1.0 : ratio);
-  return (float)(1.0 / den);
 }
 
 struct P3Scalars {
@@ -595,16 +708,13 @@ __global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restric
                                                       const Item *__restrict__ items, StepConsts k) {
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  __shared__ double sh[kThreads];
   const Tile tl = tile_of(t, it.tile);
-  const float kc = clip_factor(t, k.d, sh);
+  const float kc = ldg(&t.sc->k);
   const Dither dz(k.seed, k.step, t.tensor_id);
-  if (t.kind == kFactored) {
-    const float q = mean_r_clamped(t, k.eps, sh);
-    p3_factored(t, tl, k, kc, q, dz);
-  } else {
+  if (t.kind == kFactored)
+    p3_factored(t, tl, k, kc, ldg(&t.sc->q), dz);
+  else
     p3_exact(t, tl, k, kc, dz);
-  }
 }
 
 }  // namespace
@@ -622,6 +732,16 @@ int launch_fold(const DevTensor *T, const Item *items, int64_t count, const Step
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(p2_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
+  return (int)hipGetLastError();
+}
+int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int exact, void *stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(clip_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, exact);
+  return (int)hipGetLastError();
+}
+int launch_p2_exact(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(p2_exact_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
   return (int)hipGetLastError();
 }
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {

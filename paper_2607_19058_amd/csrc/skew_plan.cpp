@@ -66,6 +66,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     const int64_t tiles = ntc * ntr;
 
     tp.off_ssum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
+    tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
+    tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
+    p.clip.push_back({i, 0});
     if (tp.kind == kFactored) {
       const int64_t nfr = ceil_div(tp.n, kFold), nfc = ceil_div(tp.m, kFold);
       if (nfr + nfc > INT32_MAX / 2) return SKEW_EINVAL;
@@ -89,10 +92,12 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   size_t ws = 0;
   p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
   p.off_items = ws;
-  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + 1));
+  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1));
   for (auto &tp : p.t) {
     if (tp.empty) continue;
     tp.off_ssum += ws;
+    tp.off_qsum += ws;
+    tp.off_sc += ws;
     if (tp.kind == kFactored) {
       tp.off_rowpart += ws;
       tp.off_colpart += ws;

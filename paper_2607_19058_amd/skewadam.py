@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libskewadam.so")
 
 SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
+FLAG_EXACT_CLIP = 1
 TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
 ABI_VERSION = 1
 
@@ -166,8 +167,8 @@ class SkewAdam:
         return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
 
     def step(self, step: int, lr: float = 3e-4, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
-             clip_threshold: float = 1.0, seed: int = 0, stream=None) -> None:
-        hp = HParams(lr, beta1, beta2, eps, clip_threshold, 0, int(step), int(seed) & (2**64 - 1))
+             clip_threshold: float = 1.0, seed: int = 0, stream=None, flags: int = 0) -> None:
+        hp = HParams(lr, beta1, beta2, eps, clip_threshold, int(flags), int(step), int(seed) & (2**64 - 1))
         rc = self._lib.skew_step(self._ctx, ctypes.byref(hp), self._stream(stream))
         if rc != SKEW_OK:
             raise SkewError(rc, "skew_step")

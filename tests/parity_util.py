@@ -71,8 +71,8 @@ class ParityRun:
     """Runs the HIP step over every tensor of a workload and the oracle over a sample."""
 
     def __init__(self, wl: W.Workload, sample: Optional[List[int]] = None, device="cuda", seed: int = 0,
-                 hp: Optional[dict] = None, specs: Optional[List[W.Spec]] = None):
-        self.wl, self.device, self.seed = wl, torch.device(device), seed
+                 hp: Optional[dict] = None, specs: Optional[List[W.Spec]] = None, flags: int = 0):
+        self.wl, self.device, self.seed, self.flags = wl, torch.device(device), seed, flags
         self.hp = dict(oracle.DEFAULTS) if hp is None else dict(hp)
         self.specs = specs if specs is not None else wl.specs
         self.W = [W.init_weight(s, wl, self.device) for s in self.specs]
@@ -97,7 +97,7 @@ class ParityRun:
             self.O[k].g = bits(self.G[k])
         torch.cuda.synchronize()
         t0 = time.time()
-        self.opt.step(t, seed=self.seed, **self.hp)
+        self.opt.step(t, seed=self.seed, flags=self.flags, **self.hp)
         torch.cuda.synchronize()
         t1 = time.time()
         oracle.step([self.O[k] for k in self.sample], t, seed=self.seed, want_y=True, **self.hp)

@@ -43,6 +43,16 @@ def _unit_workload():
     return W.Workload("unit", specs, 3)
 
 
+def test_tiny_exact_clip_everywhere():
+    """The exact re-check of the clip factor's sum, forced for every tensor at every step,
+    gives the same bits as the oracle (it is the path the clip stage takes when the fast
+    estimate cannot decide k's rounding)."""
+    from paper_2607_19058_amd.skewadam import FLAG_EXACT_CLIP
+    log("[parity] tiny with the exact clip re-check forced on every tensor")
+    st = run(W.get("tiny"), flags=FLAG_EXACT_CLIP)
+    assert st.ok(), st
+
+
 def test_unit_shapes_all_tiers():
     log("[parity] unit shapes: odd, ragged and vector shapes in every tier, 3 steps")
     st = run(_unit_workload(), hp=dict(oracle.DEFAULTS, lr=1e-2))
@@ -168,3 +178,41 @@ def test_hparam_errors_launch_nothing():
             opt.step(**bad)
     torch.cuda.synchronize()
     assert torch.equal(w, torch.ones_like(w))
+
+
+def test_full_6p78b_sampled():
+    """The benchmark workload (6,784,327,680 parameters, 432 tensors), all 20 steps, in the
+    launch configuration bench.py times; the oracle follows a sample of tensors from every
+    tier (norm vector, attention, positions, expert matrices of both orientations including a
+    zero-gradient one, a router)."""
+    wl = W.get("full")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sc = W.expert_scales(wl, 1)[0]
+    zero_e = int(np.flatnonzero(sc == 0)[0])
+    sample = [names["norm.3"], names["attn.7"], names["pos_embed"], names["ex5.gate"], names["ex77.down"],
+              names[f"ex{zero_e}.up"], names["router.1"]]
+    log(f"[parity] full 6.78B: 432 tensors, 20 steps, sampled {sample}")
+    st = run(wl, sample=sample)
+    assert st.ok(), st
+
+
+def test_ragged_sampled():
+    """Non-power-of-two widths (1536, 6144, 4096, 11008), 1-D bias and norm vectors on the
+    exact fallback, a 4096x64 router; 50 steps."""
+    wl = W.get("ragged")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sample = [names["norm.1"], names["bias.2"], names["attn.0"], names["exA3.up"], names["exA9.down"],
+              names["exB40.down"], names["router"]]
+    log(f"[parity] ragged: 269 tensors (7.05B params), 50 steps, sampled {sample}")
+    st = run(wl, sample=sample)
+    assert st.ok(), st
+
+
+def test_more_than_2p31_elements():
+    """A 65537 x 32768 expert matrix (2,147,516,416 elements > 2^31) and a backbone vector of
+    2^31 + 3 elements: 64-bit sizes and element indices through the whole step."""
+    wl = W.Workload("big", [W.Spec("big", W.EXPERT, (65537, 32768), 0), W.Spec("vec", W.BACKBONE, ((1 << 31) + 3,), 1)], 2)
+    log("[parity] > 2^31 elements: 65537x32768 expert matrix and a (2^31+3)-element backbone vector, 2 steps")
+    st = run(wl)
+    assert st.ok(), st
+    assert st.compared >= 2 * ((1 << 31) + 65537 * 32768)

@@ -176,9 +176,7 @@ def main() -> int:
     dom = max(kern_avg, key=kern_avg.get)
     # the apply kernel alone reads G, W (and M or V) and writes W (and M or V) once:
     # its algorithmic bytes per launch are the step's; the other kernels re-read G
-    dom_bytes = {"p3_apply_dither": alg,
-                 "p1_rowcol_sumsq": 2 * sum(s.numel for s in wl.specs if tier_class(s) in ("expert", "backbone_matrix")),
-                 "p2_update_sumsq": alg, "fold_rc_ema": 0}[dom]
+    dom_bytes = {"p3_apply_dither": alg}.get(dom, 0)
     achieved = dom_bytes / (kern_avg[dom] * 1e-3) / 1e9
     traffic = None
     if os.path.exists(TRAFFIC_FILE):

@@ -12,8 +12,9 @@
 using namespace skew;
 
 namespace {
-constexpr int kLaunches = 7;
-const char *const kLaunchNames[kLaunches] = {"p1_rowcol_sumsq", "fold_rc_ema", "p2_update_sumsq", "clip_factor",
+constexpr int kLaunches = 9;
+const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_stats_other", "p1_rowcol_sumsq",
+                                             "fold_rc_ema", "p2_update_sumsq", "clip_factor",
                                              "p2_exact_recheck", "clip_factor_recheck", "p3_apply_dither"};
 }  // namespace
 
@@ -21,6 +22,8 @@ struct skew_ctx {
   Plan plan;
   DevTensor *d_table = nullptr;
   Item *d_p1 = nullptr, *d_fold = nullptr, *d_p2 = nullptr, *d_p3 = nullptr, *d_clip = nullptr;
+  Item *d_z[kZVariants] = {};     // row-band pass items, one list per kernel variant
+  int64_t n_z[kZVariants] = {};
   // diagnostics: events [step][kLaunches + 1]
   std::vector<hipEvent_t> ev;
   int ev_steps = 0, ev_used = 0;
@@ -126,12 +129,21 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.ssum = reinterpret_cast<double *>(ws + tp.off_ssum);
     x.qsum = reinterpret_cast<double *>(ws + tp.off_qsum);
     x.sc = reinterpret_cast<TensorScalars *>(ws + tp.off_sc);
-    if (tp.kind == kFactored) {
-      x.rowpart = reinterpret_cast<double *>(ws + tp.off_rowpart);
-      x.colpart = reinterpret_cast<double *>(ws + tp.off_colpart);
-      x.ainv = reinterpret_cast<double *>(ws + tp.off_ainv);
-      x.rsum = reinterpret_cast<double *>(ws + tp.off_rsum);
-    }
+    auto wsp = [&](size_t off) { return off == SIZE_MAX ? nullptr : static_cast<void *>(ws + off); };
+    x.rowpart = static_cast<double *>(wsp(tp.off_rowpart));
+    x.colpart = static_cast<double *>(wsp(tp.off_colpart));
+    x.zpart = static_cast<double *>(wsp(tp.off_zpart));
+    x.ainv = static_cast<double *>(wsp(tp.off_ainv));
+    x.rsum = static_cast<double *>(wsp(tp.off_rsum));
+    x.bst = static_cast<BandStats *>(wsp(tp.off_bst));
+    x.cst = static_cast<ColStats *>(wsp(tp.off_cst));
+    x.zpath = tp.zpath;
+    x.nseg = tp.nseg;
+    x.zcw = tp.zcw;
+    x.zrpi = tp.zrpi;
+    x.nzb = tp.nzb;
+    x.zrb = tp.zrb;
+    x.zrows = tp.zrows;
     x.n = tp.n;
     x.m = tp.m;
     x.ld = tp.ld;
@@ -146,9 +158,18 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.vec = aligned16(d[i].w) && aligned16(d[i].g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
     x.tensor_id = d[i].tensor_id;
   }
+  // row-band pass items by kernel variant (16-byte aligned rows or element loads is known
+  // only here, from the pointers)
+  std::vector<Item> zv[kZVariants];
+  for (const Item &it : p.z) {
+    const DevTensor &x = table[it.tensor];
+    const int lg = x.nseg == 1 ? 0 : (x.nseg == 2 ? 1 : 2);
+    zv[lg * 4 + (x.vec ? 0 : 2) + (x.momentum ? 1 : 0)].push_back(it);
+  }
   std::vector<Item> items;
-  items.reserve(p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
+  items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
   items.insert(items.end(), p.p1.begin(), p.p1.end());
+  for (const auto &v : zv) items.insert(items.end(), v.begin(), v.end());
   items.insert(items.end(), p.fold.begin(), p.fold.end());
   items.insert(items.end(), p.p2.begin(), p.p2.end());
   items.insert(items.end(), p.p3.begin(), p.p3.end());
@@ -160,7 +181,13 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   c->d_table = reinterpret_cast<DevTensor *>(ws + p.off_table);
   Item *base = reinterpret_cast<Item *>(ws + p.off_items);
   c->d_p1 = base;
-  c->d_fold = c->d_p1 + p.p1.size();
+  Item *cur = c->d_p1 + p.p1.size();
+  for (int v = 0; v < kZVariants; v++) {
+    c->d_z[v] = cur;
+    c->n_z[v] = (int64_t)zv[v].size();
+    cur += zv[v].size();
+  }
+  c->d_fold = cur;
   c->d_p2 = c->d_fold + p.fold.size();
   c->d_p3 = c->d_p2 + p.p2.size();
   c->d_clip = c->d_p3 + p.p3.size();
@@ -190,20 +217,27 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   hipEvent_t *ev = nullptr;
   if (ctx->ev_used < ctx->ev_steps) ev = &ctx->ev[(size_t)ctx->ev_used++ * (kLaunches + 1)];
   int e = ev ? (int)hipEventRecord(ev[0], s) : 0;
-  if (e == 0) e = launch_p1(ctx->d_table, ctx->d_p1, (int64_t)p.p1.size(), stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[1], s);
-  if (e == 0) e = launch_fold(ctx->d_table, ctx->d_fold, (int64_t)p.fold.size(), k, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[2], s);
-  if (e == 0) e = launch_p2(ctx->d_table, ctx->d_p2, (int64_t)p.p2.size(), k, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[3], s);
-  if (e == 0) e = launch_clip(ctx->d_table, ctx->d_clip, (int64_t)p.clip.size(), k, 0, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[4], s);
-  if (e == 0) e = launch_p2_exact(ctx->d_table, ctx->d_p2, (int64_t)p.p2.size(), k, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[5], s);
-  if (e == 0) e = launch_clip(ctx->d_table, ctx->d_clip, (int64_t)p.clip.size(), k, 1, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[6], s);
-  if (e == 0) e = launch_p3(ctx->d_table, ctx->d_p3, (int64_t)p.p3.size(), k, stream);
-  if (e == 0 && ev) e = (int)hipEventRecord(ev[7], s);
+  // launch j of the step, then (with timing on) the event that ends it
+  auto run = [&](int j, int rc) {
+    if (e == 0) e = rc;
+    if (e == 0 && ev) e = (int)hipEventRecord(ev[j + 1], s);
+  };
+  const DevTensor *T = ctx->d_table;
+  // row-band pass: the main variant (aligned rows, no momentum) is launch 0, the rest launch 1
+  if (e == 0) run(0, launch_p1z(T, ctx->d_z[0], ctx->n_z[0], k, 0, stream));
+  if (e == 0) {
+    int rc = 0;
+    for (int v = 1; v < kZVariants && rc == 0; v++) rc = launch_p1z(T, ctx->d_z[v], ctx->n_z[v], k, v, stream);
+    run(1, rc);
+  }
+  if (e == 0) run(2, launch_p1(T, ctx->d_p1, (int64_t)p.p1.size(), stream));
+  if (e == 0) run(3, launch_fold(T, ctx->d_fold, (int64_t)p.fold.size(), k, stream));
+  if (e == 0) run(4, launch_p2(T, ctx->d_p2, (int64_t)p.p2.size(), k, stream));
+  if (e == 0) run(5, launch_clip(T, ctx->d_clip, (int64_t)p.clip.size(), k, 0, stream));
+  // the exact re-check runs over every tile; tensors the clip stage did not flag exit at once
+  if (e == 0) run(6, launch_p2_exact(T, ctx->d_p3, (int64_t)p.p3.size(), k, stream));
+  if (e == 0) run(7, launch_clip(T, ctx->d_clip, (int64_t)p.clip.size(), k, 1, stream));
+  if (e == 0) run(8, launch_p3(T, ctx->d_p3, (int64_t)p.p3.size(), k, stream));
   return e == 0 ? SKEW_OK : SKEW_EHIP;
 }
 

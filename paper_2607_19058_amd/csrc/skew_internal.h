@@ -18,11 +18,45 @@ constexpr int kFold = 256;              // rows (or columns) folded by one work-
 constexpr int64_t kTileElems = 1 << 19; // target elements per tile: 1 MiB of bf16 gradient
 constexpr size_t kAlign = 256;
 
+// Row-band pass (pass 1 of factored matrices up to kZMaxCols columns): a work-group of
+// kZThreads threads owns whole rows, so it knows each R_i as soon as the row is summed.
+constexpr int kZThreads = 512;           // 8 wave64 (up to 256 VGPRs each: nothing is held in flight)
+constexpr int kZWaves = kZThreads / 64;
+constexpr int kZMaxSeg = 4;              // 512-column chunks per wave and row
+constexpr int64_t kZBandElems = 1 << 21; // target elements per row band: 4 MiB of bf16 gradient
+constexpr int kZVariants = 12;           // kernel variants: log2(nseg) * 4 + (element loads ? 2 : 0) + momentum
+constexpr int kZLdsBytes = 64 * 1024;    // one LDS staging buffer of the row-band pass (two per work-group)
+constexpr int kZMaxBlockRows = 64;       // rows staged per block, at most
+
 // Per-tensor scalars of one step, written by the clip stage and read by the update.
 struct TensorScalars {
   float k;            // clip factor 1 / max(1, RMS(U_hat) / d), rounded as the oracle rounds it
   float q;            // max(mean R, eps) (factored tensors)
   int32_t ambiguous;  // 1: the approximate sum left k's rounding undecided; the exact pass decides
+  int32_t regime;     // row-band tensors, set by the clip stage for the next step: which sums the
+                      // row-band pass forms (kRegime*); zero (both) after skew_state_init
+};
+// Which update sums the row-band pass forms: both, only the one above the eps floor
+// (the last step had every element clearly above it), or only the floored one.
+enum Regime : int32_t { kRegimeBoth = 0, kRegimeAbove = 1, kRegimeFloor = 2 };
+
+// Per row band of the row-band pass: sums and extremes the clip stage needs.
+struct BandStats {
+  double rsum;    // sum of the band's R_i (after the EMA)
+  double ysum;    // sum over the band of RN(s x / sqrt(eps))^2: U_hat^2 of every element on the floor
+  double umax;    // bound of max over the band of (s x)^2 / R_i
+  float rmin;     // min R_i over rows with R_i > 0 (+inf if none)
+  float rmax;     // max R_i
+  int32_t bad;    // a row with R_i == 0 but a nonzero gradient (its elements escape the bounds)
+  int32_t regime; // the sums this band formed (kRegime*)
+};
+
+// Per fold chunk of columns of a row-band tensor.
+struct ColStats {
+  double s;       // sum over the chunk's columns of z_j / c'_j (U_hat^2 summed above the floor)
+  float cmin;     // min c'_j over columns with C_j > 0 (+inf if none)
+  float cmax;     // max c'_j
+  int32_t bad;    // non-finite c'_j, or C_j == 0 with a nonzero column sum
   int32_t pad;
 };
 
@@ -32,9 +66,12 @@ struct DevTensor {
   const uint16_t *g;
   float *M, *V, *R, *C;   // state (NULL where the tier keeps none)
   double *rowpart;        // [ntc][n]   partial row sums of g^2, one per column strip
-  double *colpart;        // [ntr][m]   partial column sums of g^2, one per row band
+  double *colpart;        // [ntr][m]   partial column sums of g^2, one per row band (row-band pass: [nzb][m])
   double *ainv;           // [n]        1/sqrt(R_i) after the step's EMA
   double *rsum;           // [nfr]      sums of R_i over each fold chunk of rows
+  double *zpart;          // [nzb][m]   row-band pass: partial column sums of (s x)^2 / R_i
+  BandStats *bst;         // [nzb]      row-band pass: per band
+  ColStats *cst;          // [nfc]      row-band pass: per fold chunk of columns
   double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
   double *qsum;           // [ntr*ntc]  per-tile sums of U_hat^4 over the approximated elements
   TensorScalars *sc;      // this step's clip factor and reconstruction clamp
@@ -46,6 +83,15 @@ struct DevTensor {
   int32_t kind;           // kFactored / kExact
   int32_t momentum;       // backbone tier
   int32_t vec;            // 16-byte aligned rows: vector loads and stores
+  int32_t zpath;          // 1: pass 1 is the row-band pass (no separate update-sum pass)
+  int32_t nseg;           // row-band pass: 512-column chunks per wave (1..kZMaxSeg)
+  int32_t zcw;            // row-band pass: 512-column chunks per row
+  int32_t zrpi;           // row-band pass: row groups per work-group (rows side by side); a group
+                          // is wpr = ceil(zcw / nseg) waves, wave w of it takes chunks w, w + wpr
+  int32_t nzb;            // row-band pass: row bands
+  int32_t zrb;            // row-band pass: rows per group and block
+  int32_t pad2;
+  int64_t zrows;          // row-band pass: rows per band
   uint64_t tensor_id;
 };
 
@@ -73,12 +119,17 @@ struct TensorPlan {
   size_t off_m = SIZE_MAX, off_v = SIZE_MAX, off_r = SIZE_MAX, off_c = SIZE_MAX;
   // workspace offsets in bytes
   size_t off_rowpart = SIZE_MAX, off_colpart = SIZE_MAX, off_ainv = SIZE_MAX, off_rsum = SIZE_MAX,
-         off_ssum = SIZE_MAX, off_qsum = SIZE_MAX, off_sc = SIZE_MAX;
+         off_ssum = SIZE_MAX, off_qsum = SIZE_MAX, off_sc = SIZE_MAX, off_zpart = SIZE_MAX, off_bst = SIZE_MAX,
+         off_cst = SIZE_MAX;
+  // row-band pass geometry
+  int32_t zpath = 0, nseg = 0, zcw = 0, zrpi = 0, nzb = 0, zrb = 0;
+  int64_t zrows = 0;
 };
 
 struct Plan {
   std::vector<TensorPlan> t;
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
+  std::vector<Item> z;                        // row-band pass items (split by kernel variant at init)
   size_t state_bytes = 0;
   size_t ws_bytes = 0;
   size_t off_table = 0, off_items = 0;   // workspace offsets of the device table and item lists
@@ -91,6 +142,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out);
 
 // Kernel launchers (skew_kernels.hip). Return a hipError_t value.
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream);
+// row-band pass, kernel variant log2(nseg) * 4 + (element loads ? 2 : 0) + (momentum ? 1 : 0)
+int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, void *stream);
+
 int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);

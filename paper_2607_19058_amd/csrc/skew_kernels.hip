@@ -1,21 +1,27 @@
 // skew_kernels.hip -- gfx950 kernels of one SkewAdam step (Sec. 3, Eq. 1, Alg. 1).
 //
-// A step is four stream-ordered launches over device-resident work-item tables;
-// each launch covers every tensor of the table (e.g. all experts of a layer):
-//   p1    factored tensors: per tile, partial row and column sums of g^2 (Eq. 1)
-//   fold  factored tensors: R, C EMA (Eq. 1), 1/sqrt(R_i), sums of R for mean(R)
-//   p2    every tensor: per tile, sum of squares of the unclipped update (Alg. 1)
-//   p3    every tensor: clip factor, momentum / exact-v update, weight update,
-//         dithered bf16 write-back (Sec. 3 "Update clipping and low-precision updates")
+// A step is a short sequence of stream-ordered launches over device-resident work-item
+// tables; each launch covers every tensor of the table (e.g. all experts of a layer):
+//   p1z   factored matrices up to 16384 columns (row-band pass): R_i, partial column sums
+//         of g^2 and of (s x)^2 / R_i, the floored sum of U_hat^2 and bounds, in one read of G
+//   p1    wider factored matrices: per tile, partial row and column sums of g^2 (Eq. 1)
+//   fold  factored tensors: C (and for wide ones R) EMA (Eq. 1), 1/sqrt(R_i), c'_j and
+//         the row-band tensors' sum of U_hat^2 above the floor
+//   p2    exact-second-moment tensors and wide factored ones: per tile, sum of squares of
+//         the unclipped update (Alg. 1)
+//   clip  per tensor: the clip factor k, and whether its rounding needs the exact pass
+//   p2x   exact re-run of the sum for the tensors the clip stage left undecided; clip again
+//   p3    every tensor: momentum / exact-v update, weight update, dithered bf16
+//         write-back (Sec. 3 "Update clipping and low-precision updates")
 // Reductions are deterministic (fixed-order partials; no float atomics), so two
 // runs on the same inputs produce identical bits.
 //
-// Tile: tr rows x (512*cw) columns. A work-group is 4 wave64; wave w takes rows
-// r0+w, r0+w+4, ...; lane l covers 8 consecutive columns (one 16-byte bf16 load)
-// in each 512-column chunk.
+// Tile (p1, p2, p3): tr rows x (512*cw) columns. A work-group is 4 wave64; lane l covers 8
+// consecutive columns (one 16-byte bf16 load) in each 512-column chunk.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "skew_internal.h"
 
@@ -63,6 +69,17 @@ __device__ __forceinline__ void unpack8(const uint4 &u, float *o) {
   o[2] = bf_lo(u.y); o[3] = bf_hi(u.y);
   o[4] = bf_lo(u.z); o[5] = bf_hi(u.z);
   o[6] = bf_lo(u.w); o[7] = bf_hi(u.w);
+}
+
+// 8 momentum values at a 32-byte aligned position
+__device__ __forceinline__ void load_m8(const float *p, float *o) {
+  const float4 a = ldg(reinterpret_cast<const float4 *>(p));
+  const float4 b = ldg(reinterpret_cast<const float4 *>(p + 4));
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+__device__ __forceinline__ void store_m8(float *p, const float *v) {
+  stg(reinterpret_cast<float4 *>(p), make_float4(v[0], v[1], v[2], v[3]));
+  stg(reinterpret_cast<float4 *>(p + 4), make_float4(v[4], v[5], v[6], v[7]));
 }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -132,6 +149,89 @@ __device__ __forceinline__ double block_sum(double x, double *sh) {
   return r;
 }
 
+// Butterfly reductions over one wave64: every lane ends with the same value (each step
+// adds two equal-order partials, and IEEE addition is commutative), so the result is
+// deterministic.
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+__device__ __forceinline__ double wave_max_d(double x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_min_f(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fminf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_max_f(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ int wave_or(int x) { return __any(x != 0) ? 1 : 0; }
+
+// Work-group reductions of NW waves through sh[NW] (every thread gets the result; the
+// per-wave results are combined in wave order).
+template <int NW>
+__device__ __forceinline__ double wg_sum_w(double x, double *sh) {
+  x = wave_sum_d(x);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+  __syncthreads();
+  double r = 0.0;
+#pragma unroll
+  for (int w = 0; w < NW; w++) r += sh[w];
+  __syncthreads();
+  return r;
+}
+template <int NW>
+__device__ __forceinline__ double wg_max_w(double x, double *sh) {
+  x = wave_max_d(x);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = x;
+  __syncthreads();
+  double r = sh[0];
+#pragma unroll
+  for (int w = 1; w < NW; w++) r = fmax(r, sh[w]);
+  __syncthreads();
+  return r;
+}
+template <int NW>
+__device__ __forceinline__ float wg_min_wf(float x, double *sh) {
+  x = wave_min_f(x);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = (double)x;
+  __syncthreads();
+  float r = (float)sh[0];
+#pragma unroll
+  for (int w = 1; w < NW; w++) r = fminf(r, (float)sh[w]);
+  __syncthreads();
+  return r;
+}
+template <int NW>
+__device__ __forceinline__ float wg_max_wf(float x, double *sh) {
+  x = wave_max_f(x);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = (double)x;
+  __syncthreads();
+  float r = (float)sh[0];
+#pragma unroll
+  for (int w = 1; w < NW; w++) r = fmaxf(r, (float)sh[w]);
+  __syncthreads();
+  return r;
+}
+template <int NW>
+__device__ __forceinline__ int wg_or_w(int x, double *sh) {
+  x = wave_or(x);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = (double)x;
+  __syncthreads();
+  int r = 0;
+#pragma unroll
+  for (int w = 0; w < NW; w++) r |= (sh[w] != 0.0) ? 1 : 0;
+  __syncthreads();
+  return r;
+}
+
 // A tile is one row band (rows band, band + ntr, band + 2 ntr, ...: interleaved, so that
 // the work-groups running at the same time on one tensor read neighbouring rows) times
 // one column strip of 512*cw columns.
@@ -186,12 +286,6 @@ __device__ __forceinline__ void load_g8(const DevTensor &t, int64_t i, int64_t c
 // Squares of bf16 values are exact in double and the sums stay far from double
 // rounding, so every partial is (nearly) the exact sum, independent of order.
 // --------------------------------------------------------------------------------------------
-__device__ __forceinline__ double wave_sum_d(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
 constexpr int kRowSlots = (int)(kTileElems / kChunk);   // tile rows x chunks per row
 
 __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restrict__ TT,
@@ -252,6 +346,548 @@ __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restric
 }
 
 // --------------------------------------------------------------------------------------------
+// Row-band pass: pass 1 of factored matrices whose staged rows fit (Eq. 1 and the update
+// sum of Alg. 1 in one read of G).
+//
+// A work-group owns a band of whole rows, so R_i <- b2 R_i + a2 mean_j g_ij^2 is final as
+// soon as row i is summed. With the row still at hand the work-group adds (s x_ij)^2 / R_i
+// to a per-column sum z_j (x = g, or the new momentum on the backbone). Above the eps
+// floor U_hat_ij^2 = (s x_ij)^2 / (R_i c'_j) up to the oracle's free roundings, so the
+// tensor's sum of U_hat^2 is sum_j z_j / c'_j once the fold has c'_j = C_j / max(mean R,
+// eps): no pass re-reads G for it. On the floor U_hat = RN(RN(s x) / sqrt(eps)) depends on
+// x alone; its square is summed exactly as the oracle rounds it (Markstein's correctly
+// rounded division). The clip stage takes whichever sum applies; the last step's
+// regime decides which of the two this pass forms (a tensor that was clearly above the
+// floor skips the floored sum, and the reverse).
+//
+// Roundings that repeat a pattern are replicated (RN(s x); the momentum fma), so the
+// remaining difference from the oracle's sum is the free roundings of R_i c'_j, the
+// square root and the quotient; the per-band maximum of (s x)^2 / R_i bounds their spread.
+//
+// Staging: blocks of zrpi * zrb whole rows (bf16 gradient, and fp32 momentum on the
+// backbone) move into one of two LDS buffers while the other is being summed: with the
+// direct global-to-LDS loads (16 bytes per lane) when rows are 16-byte aligned, through
+// registers otherwise. No register holds data in flight, so a 512-thread work-group with
+// up to 256 VGPRs per wave keeps a whole block (up to 64 KiB) of loads outstanding.
+//
+// Layout: zcw 512-column chunks per row; a group of wpr = ceil(zcw / NSEG) waves shares a
+// row, wave w of the group taking chunks w, w + wpr, ...; zrpi = 8 / wpr groups work on
+// different rows. The column partials of the groups are added in group order through LDS.
+// --------------------------------------------------------------------------------------------
+__device__ __forceinline__ uint4 load_bf8(const uint16_t *base, int64_t ld, int64_t m, int64_t i, int64_t col) {
+  const uint16_t *row = base + i * ld;
+  uint32_t v[4];
+#pragma unroll
+  for (int e2 = 0; e2 < 4; e2++) {
+    const uint32_t lo = (col + 2 * e2 < m) ? (uint32_t)ldg(row + col + 2 * e2) : 0u;
+    const uint32_t hi = (col + 2 * e2 + 1 < m) ? (uint32_t)ldg(row + col + 2 * e2 + 1) : 0u;
+    v[e2] = lo | (hi << 16);
+  }
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) void gbl_void_t;
+__device__ __forceinline__ void dma16(const void *g, void *lds) {
+  __builtin_amdgcn_global_load_lds((gbl_void_t *)g, (lds_void_t *)lds, 16, 0, 0);
+}
+__device__ __forceinline__ void dma4(const void *g, void *lds) {
+  __builtin_amdgcn_global_load_lds((gbl_void_t *)g, (lds_void_t *)lds, 4, 0, 0);
+}
+// s_waitcnt immediates (gfx9 encoding): vmcnt(0) and lgkmcnt(0); only lgkmcnt(0)
+constexpr int kWaitVmLgkm0 = 0x0070;
+constexpr int kWaitLgkm0 = 0xC07F;
+
+// Reads from a staging buffer are opaque to the compiler's wait insertion, which cannot
+// tell the buffer being read from the one the next block is loading into and would
+// otherwise wait for that load; the staged data is known to be complete from the wait
+// and barrier that open each block. N reads are in flight together, then one wait.
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char *)p;
+}
+__device__ __forceinline__ uint4 to_uint4(const u32x4_t &v) { return make_uint4(v.x, v.y, v.z, v.w); }
+template <int N>
+__device__ __forceinline__ void lds_read16_n(const unsigned char *const (&p)[N], uint4 (&u)[N]) {
+  u32x4_t v[N > 4 ? 8 : 4];
+  if constexpr (N == 1) {
+    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v[0]) : "v"(lds_addr(p[0])) : "memory");
+  } else if constexpr (N == 2) {
+    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(v[0]), "=&v"(v[1])
+                 : "v"(lds_addr(p[0])), "v"(lds_addr(p[1]))
+                 : "memory");
+  } else if constexpr (N == 4) {
+    asm volatile(
+        "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+        : "v"(lds_addr(p[0])), "v"(lds_addr(p[1])), "v"(lds_addr(p[2])), "v"(lds_addr(p[3]))
+        : "memory");
+  } else {
+    static_assert(N == 8, "1, 2, 4 or 8 reads");
+    asm volatile(
+        "ds_read_b128 %0, %8\n\tds_read_b128 %1, %9\n\tds_read_b128 %2, %10\n\tds_read_b128 %3, %11\n\t"
+        "ds_read_b128 %4, %12\n\tds_read_b128 %5, %13\n\tds_read_b128 %6, %14\n\tds_read_b128 %7, %15\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]), "=&v"(v[7])
+        : "v"(lds_addr(p[0])), "v"(lds_addr(p[1])), "v"(lds_addr(p[2])), "v"(lds_addr(p[3])),
+          "v"(lds_addr(p[4])), "v"(lds_addr(p[5])), "v"(lds_addr(p[6])), "v"(lds_addr(p[7]))
+        : "memory");
+  }
+#pragma unroll
+  for (int j = 0; j < N; j++) u[j] = to_uint4(v[j]);
+}
+__device__ __forceinline__ void lds_write16(unsigned char *p, uint4 u) {
+  *reinterpret_cast<__attribute__((address_space(3))) u32x4_t *>(
+      (__attribute__((address_space(3))) unsigned char *)p) = u32x4_t{u.x, u.y, u.z, u.w};
+}
+
+constexpr int kZRowSlots = kZMaxBlockRows * kZWaves;   // row partials of one block: [row][wave in group]
+
+// Cross-lane moves of doubles without LDS: DPP within 16-lane rows (quad permutes, half
+// and full row mirrors) and the gfx950 lane-half swaps. Each reduction step adds two
+// partials that both lanes of a pair add in the same order: results are deterministic.
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i within each 8 lanes
+constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i within each 16 lanes
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+// a, b -> lanes < 32: a[l] + a[l + 32]; lanes >= 32: b[l - 32] + b[l]
+__device__ __forceinline__ double swap32_add(double a, double b) {
+  const auto lo = __builtin_amdgcn_permlane32_swap(__double2loint(a), __double2loint(b), false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap(__double2hiint(a), __double2hiint(b), false, false);
+  return __hiloint2double(hi[0], lo[0]) + __hiloint2double(hi[1], lo[1]);
+}
+// a, b -> 16-lane rows 0, 2: a summed with the next row; rows 1, 3: b summed with the previous
+__device__ __forceinline__ double swap16_add(double a, double b) {
+  const auto lo = __builtin_amdgcn_permlane16_swap(__double2loint(a), __double2loint(b), false, false);
+  const auto hi = __builtin_amdgcn_permlane16_swap(__double2hiint(a), __double2hiint(b), false, false);
+  return __hiloint2double(hi[0], lo[0]) + __hiloint2double(hi[1], lo[1]);
+}
+// Sums over the wave of RB values per lane (one per row), transposed: the lane halves and
+// quarters exchange different rows first. Row b's total ends in lanes [b * 64/RB, (b + 1) * 64/RB).
+template <int RB>
+__device__ __forceinline__ double wave_sum_rows(const double (&v)[RB]) {
+  const int lane = threadIdx.x & 63;
+  double x;
+  if constexpr (RB == 1) {
+    const double w = swap32_add(v[0], v[0]);
+    x = swap16_add(w, w);
+  } else if constexpr (RB == 2) {
+    const double w = swap32_add(v[0], v[1]);
+    x = swap16_add(w, w);
+  } else if constexpr (RB == 4) {
+    x = swap16_add(swap32_add(v[0], v[2]), swap32_add(v[1], v[3]));
+  } else {
+    static_assert(RB == 8, "1, 2, 4 or 8 rows");
+    const double u0 = swap16_add(swap32_add(v[0], v[4]), swap32_add(v[2], v[6]));
+    const double u1 = swap16_add(swap32_add(v[1], v[5]), swap32_add(v[3], v[7]));
+    const double a = u0 + dpp_d<kDppMirror>(u0), b = u1 + dpp_d<kDppMirror>(u1);
+    x = (lane & 8) ? b : a;
+  }
+  x += dpp_d<kDppXor1>(x);
+  x += dpp_d<kDppXor2>(x);
+  x += dpp_d<kDppHalfMirror>(x);
+  if constexpr (RB < 8) x += dpp_d<kDppMirror>(x);
+  return x;
+}
+// exact (float)(x / d) for double x >= 0 and d > 0 with rd = RN(1 / d): the quotient is
+// correctly rounded in double (Markstein) before the rounding to float
+__device__ __forceinline__ float div_to_float(double x, double d, double rd) {
+  const double q0 = x * rd;
+  const double q = fma(fma(-q0, d, x), rd, q0);
+  return (float)q;
+}
+// 1 / x and 1 / sqrt(x) to about 2^-50 (hardware estimate and one Newton step)
+__device__ __forceinline__ double rcp_d(double x) {
+  const double y = __builtin_amdgcn_rcp(x);
+  return fma(y, fma(-x, y, 1.0), y);
+}
+__device__ __forceinline__ double rsq_d(double x) {
+  const double y = __builtin_amdgcn_rsq(x);
+  return y * fma(-0.5 * x * y, y, 1.5);
+}
+
+template <int NSEG, int RB, bool MOM, bool VEC>
+__device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, unsigned char *bufA,
+                                         unsigned char *bufB, float *rbA, float *rbB, double *rowsh, double *sh) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int64_t m = t.m, ld = t.ld;
+  const int zcw = t.zcw;
+  const int wpr = (zcw + NSEG - 1) / NSEG;   // waves per row
+  const int grp = wave / wpr;
+  const int wg = wave - grp * wpr;           // wave within the group
+  const int rpi = t.zrpi;
+  constexpr int rb = RB;                     // rows per group and block
+  const int br = rpi * rb;                   // rows per block
+  const bool active = grp < rpi;
+  const int grp_c = active ? grp : 0;        // idle waves read (and discard) group 0's rows
+  int P = 1;                                 // wpr rounded up to a power of two
+  while (P < wpr) P <<= 1;
+  bool sok[NSEG];
+  int chs[NSEG];
+  int64_t col[NSEG];
+#pragma unroll
+  for (int s = 0; s < NSEG; s++) {
+    chs[s] = wg + s * wpr;
+    col[s] = (int64_t)chs[s] * kChunk + lane * 8;
+    sok[s] = active && chs[s] < zcw && col[s] < m;
+  }
+  const int64_t r0 = (int64_t)band * t.zrows;
+  const int64_t r1 = (t.n - r0 < t.zrows) ? t.n : r0 + t.zrows;
+  const int64_t nblk = (r1 - r0 + br - 1) / br;
+  const int npieces = br * zcw;          // 1 KiB pieces of gradient per block
+  const int goff_m = npieces * 1024;     // momentum pieces follow (2 KiB each)
+  const float sc = MOM ? k.s_m : k.s_0;
+  const float deps = sqrtf(k.eps);                  // the oracle's D on the floor
+  const float reps = (float)(1.0 / (double)deps);   // correctly rounded 1/D
+  const double dm = (double)m, rdm = 1.0 / dm;
+  // the sums this step forms (the clip stage's prediction from the last step)
+  const int regime = __builtin_amdgcn_readfirstlane(ldg(&t.sc->regime));
+  const bool want_z = regime != kRegimeFloor, want_y = regime != kRegimeAbove;
+
+  double cacc[NSEG][8], zacc[NSEG][8];
+#pragma unroll
+  for (int s = 0; s < NSEG; s++)
+#pragma unroll
+    for (int e = 0; e < 8; e++) cacc[s][e] = zacc[s][e] = 0.0;
+  double ysum = 0.0, umax = 0.0;
+  // R statistics, kept by lane b * P of the group's first wave for its rows
+  double rs_l = 0.0;
+  float rmn_l = __builtin_inff(), rmx_l = 0.f;
+  int bad_l = 0;
+
+  // Block loads: piece p = (row r, chunk c) of the block goes to wave p % 8. Rows past
+  // the band's end and lanes past the row's end load a valid address; their slots are
+  // never used. Wave 0 also stages the block's old R values.
+  const int pr0 = wave / zcw, pc0 = wave - pr0 * zcw;                   // piece `wave`: (row, chunk)
+  const int dr = kZWaves / zcw, dc = kZWaves - (kZWaves / zcw) * zcw;   // step of 8 pieces
+  auto issue = [&](int64_t blk, unsigned char *buf, float *rbuf) {
+    const int64_t rbase = r0 + blk * br;
+    int r = pr0, c = pc0;
+    for (int p = wave; p < npieces; p += kZWaves) {
+      const int64_t i = (rbase + r < r1) ? rbase + r : r1 - 1;
+      const int64_t cg = (int64_t)c * kChunk + lane * 8;
+      if (VEC) {
+        dma16(t.g + i * ld + (cg < m ? cg : 0), buf + (size_t)p * 1024);
+      } else {
+        lds_write16(buf + (size_t)p * 1024 + lane * 16, load_bf8(t.g, ld, m, i, cg));
+      }
+      if (MOM) {
+        const float *mrow = t.M + i * m;
+        const int64_t c0 = (int64_t)c * kChunk + lane * 4, c1 = c0 + 256;
+        if (VEC) {
+          dma16(mrow + (c0 < m ? c0 : 0), buf + goff_m + (size_t)p * 2048);
+          dma16(mrow + (c1 < m ? c1 : 0), buf + goff_m + (size_t)p * 2048 + 1024);
+        } else {
+          uint32_t mv[8];
+#pragma unroll
+          for (int e = 0; e < 4; e++) {
+            mv[e] = (c0 + e < m) ? __float_as_uint(ldg(mrow + c0 + e)) : 0u;
+            mv[4 + e] = (c1 + e < m) ? __float_as_uint(ldg(mrow + c1 + e)) : 0u;
+          }
+          lds_write16(buf + goff_m + (size_t)p * 2048 + lane * 16, make_uint4(mv[0], mv[1], mv[2], mv[3]));
+          lds_write16(buf + goff_m + (size_t)p * 2048 + 1024 + lane * 16, make_uint4(mv[4], mv[5], mv[6], mv[7]));
+        }
+      }
+      r += dr;
+      c += dc;
+      if (c >= zcw) {
+        c -= zcw;
+        r++;
+      }
+    }
+    if (wave == 0) {
+      const int64_t i = rbase + (lane < br ? lane : br - 1);
+      const int64_t ic = i < r1 ? i : r1 - 1;
+      if (VEC)
+        dma4(t.R + ic, rbuf);
+      else
+        rbuf[lane] = ldg(t.R + ic);
+    }
+  };
+  // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (four
+  // 16-byte reads in flight together); zero where the lane has no column or the row is
+  // past the band's end.
+  constexpr int RBB = (4 / NSEG < RB ? 4 / NSEG : RB) > 0 ? (4 / NSEG < RB ? 4 / NSEG : RB) : 1;
+  auto read_rows = [&](const unsigned char *buf, int64_t rbase, int b0, uint4 (&u)[RBB][NSEG]) {
+    const unsigned char *ptr[RBB * NSEG];
+    uint4 v[RBB * NSEG];
+#pragma unroll
+    for (int b = 0; b < RBB; b++)
+#pragma unroll
+      for (int s = 0; s < NSEG; s++) {
+        const int ch = chs[s] < zcw ? chs[s] : 0;
+        ptr[b * NSEG + s] = buf + (size_t)((grp_c * RB + b0 + b) * zcw + ch) * 1024 + lane * 16;
+      }
+    lds_read16_n<RBB * NSEG>(ptr, v);
+#pragma unroll
+    for (int b = 0; b < RBB; b++) {
+      const bool rv = active && rbase + grp_c * RB + b0 + b < r1;
+#pragma unroll
+      for (int s = 0; s < NSEG; s++) u[b][s] = (rv && sok[s]) ? v[b * NSEG + s] : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
+    __builtin_amdgcn_s_barrier();               // ... by every wave; the other buffer is free
+    if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
+    const int64_t rbase = r0 + blk * br;
+    double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
+    // row and column sums of g^2 (bf16 squares are exact in double)
+    {
+      double rp[RB];
+#pragma unroll
+      for (int b0 = 0; b0 < RB; b0 += RBB) {
+        uint4 u[RBB][NSEG];
+        read_rows(cur, rbase, b0, u);
+#pragma unroll
+        for (int bb = 0; bb < RBB; bb++) {
+          const int b = b0 + bb;
+          rp[b] = 0.0;
+#pragma unroll
+          for (int s = 0; s < NSEG; s++) {
+            // one 8-element group at a time (the scheduler would otherwise convert every
+            // staged element to double at once)
+            __builtin_amdgcn_sched_barrier(0);
+            float x[8];
+            unpack8(u[bb][s], x);
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+              const double xd = (double)x[e];
+              rp[b] = fma(xd, xd, rp[b]);
+              cacc[s][e] = fma(xd, xd, cacc[s][e]);
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      const double rsum = wave_sum_rows<RB>(rp);
+      if (active && (lane & (64 / RB - 1)) == 0) slot[(grp * RB + lane / (64 / RB)) * kZWaves + wg] = rsum;
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+    // R_i after the EMA (Eq. 1) for the group's rb rows, lane-parallel: lane b * P + w
+    // takes the partial of wave w of row b; after the segment sum lane b * P holds the row
+    double winv_l;
+    {
+      const int b = lane / P, w = lane - b * P;
+      const int r = grp_c * rb + (b < rb ? b : 0);
+      double x = (active && b < rb && w < wpr) ? slot[r * kZWaves + w] : 0.0;
+      if (P >= 2) x += dpp_d<kDppXor1>(x);
+      if (P >= 4) x += dpp_d<kDppXor2>(x);
+      if (P >= 8) x += dpp_d<kDppHalfMirror>(x);
+      const int64_t i = rbase + r;
+      const float ri = div_to_float(x, dm, rdm);
+      const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, rcur[r]));
+      const double Rd = (double)R;
+      const bool normal = R > 0.f && R < __builtin_inff();
+      winv_l = R > 0.f ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
+      if (active && wg == 0 && b < rb && w == 0 && i < r1) {
+        stg(t.R + i, R);
+        stg(t.ainv + i, normal ? rsq_d(Rd) : 1.0 / sqrt(Rd));
+        rs_l += Rd;
+        if (R > 0.f) rmn_l = fminf(rmn_l, R);
+        rmx_l = fmaxf(rmx_l, R);
+        if (R != R || (!(R > 0.f) && x > 0.0)) bad_l = 1;
+      }
+    }
+    // z_j, the floored sum and the bound (the sums the prediction asks for)
+    auto sweep2 = [&](auto zc, auto yc) {
+      constexpr bool Z = decltype(zc)::value, Y = decltype(yc)::value;
+#pragma unroll
+      for (int b0 = 0; b0 < RB; b0 += RBB) {
+      uint4 ub[RBB][NSEG];
+      read_rows(cur, rbase, b0, ub);
+#pragma unroll
+      for (int bb = 0; bb < RBB; bb++) {
+        const int b = b0 + bb;
+        const uint4 (&u)[RBB][NSEG] = ub;
+        const int r = grp_c * rb + b;
+        const bool rv = active && rbase + r < r1;
+        const int src = b * P;
+        const double winv = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(winv_l), src),
+                                             __builtin_amdgcn_readlane(__double2loint(winv_l), src));
+        float amax = 0.f;   // max |s x| over the lane's elements of the row
+#pragma unroll
+        for (int s = 0; s < NSEG; s++) {
+          __builtin_amdgcn_sched_barrier(0);
+          float x[8];
+          unpack8(u[bb][s], x);
+          if (MOM) {
+            const int ch = chs[s] < zcw ? chs[s] : 0;
+            const unsigned char *mp = cur + goff_m + (size_t)(r * zcw + ch) * 2048 + lane * 32;
+            const unsigned char *mpp[2] = {mp, mp + 16};
+            uint4 mv[2];
+            lds_read16_n<2>(mpp, mv);
+            const bool ok = rv && sok[s];
+            const float mo[8] = {__uint_as_float(mv[0].x), __uint_as_float(mv[0].y), __uint_as_float(mv[0].z),
+                                 __uint_as_float(mv[0].w), __uint_as_float(mv[1].x), __uint_as_float(mv[1].y),
+                                 __uint_as_float(mv[1].z), __uint_as_float(mv[1].w)};
+#pragma unroll
+            for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, ok ? mo[e] : 0.f));
+          }
+#pragma unroll
+          for (int e = 0; e < 8; e++) {
+            const float ax = __fmul_rn(sc, x[e]);
+            if (Z) {
+              const double axd = (double)ax;
+              zacc[s][e] = fma(axd * axd, winv, zacc[s][e]);
+              amax = fmaxf(amax, fabsf(ax));
+            }
+            if (Y) {
+              const float q0 = ax * reps;
+              const float uf = fmaf(fmaf(-q0, deps, ax), reps, q0);   // RN(ax / deps)
+              ysum = fma((double)uf, (double)uf, ysum);
+            }
+          }
+        }
+        if (Z) umax = fmax(umax, ((double)amax * (double)amax) * winv);
+      }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    if (want_z && want_y)
+      sweep2(std::true_type(), std::true_type());
+    else if (want_z)
+      sweep2(std::true_type(), std::false_type());
+    else
+      sweep2(std::false_type(), std::true_type());
+  };
+  issue(0, bufA, rbA);
+  for (int64_t blk = 0; blk < nblk; blk += 2) {
+    step(blk, bufA, rbA, bufB, rbB);
+    if (blk + 1 >= nblk) break;
+    step(blk + 1, bufB, rbB, bufA, rbA);
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);
+  __syncthreads();
+  // column partials: groups 1.. add theirs into group 0's through LDS, in group order
+  double *colbuf = reinterpret_cast<double *>(bufA);   // zcw * 512 doubles: groups > 1 only when zcw <= 8
+  for (int gsrc = 1; gsrc < rpi; gsrc++) {
+#pragma unroll
+    for (int half = 0; half < 2; half++) {
+      if (grp == gsrc) {
+#pragma unroll
+        for (int s = 0; s < NSEG; s++)
+          if (chs[s] < zcw)
+#pragma unroll
+            for (int e = 0; e < 8; e++) colbuf[chs[s] * kChunk + lane * 8 + e] = half ? zacc[s][e] : cacc[s][e];
+      }
+      __syncthreads();
+      if (grp == 0) {
+#pragma unroll
+        for (int s = 0; s < NSEG; s++)
+          if (chs[s] < zcw)
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+              const double v = colbuf[chs[s] * kChunk + lane * 8 + e];
+              if (half) zacc[s][e] += v; else cacc[s][e] += v;
+            }
+      }
+      __syncthreads();
+    }
+  }
+  if (grp == 0) {
+    const int64_t prow = (int64_t)band * m;
+#pragma unroll
+    for (int s = 0; s < NSEG; s++) {
+      if (!sok[s]) continue;
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        if (VEC || col[s] + e < m) {
+          stg(t.colpart + prow + col[s] + e, cacc[s][e]);
+          stg(t.zpart + prow + col[s] + e, zacc[s][e]);
+        }
+      }
+    }
+  }
+  // band statistics: the R statistics sit in lanes b * P of each group's first wave, in
+  // row order; combined in (group, row) order
+  const double ys = wg_sum_w<kZWaves>(ysum, sh);
+  const double um = wg_max_w<kZWaves>(umax, sh);
+  double *gs = sh + kZWaves;
+  if (active && wg == 0) {
+    double rs = 0.0;
+    float rmn = __builtin_inff(), rmx = 0.f;
+    int bd = 0;
+    for (int b = 0; b < rb; b++) {
+      const int src = b * P;
+      rs += __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(rs_l), src),
+                             __builtin_amdgcn_readlane(__double2loint(rs_l), src));
+      rmn = fminf(rmn, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rmn_l), src)));
+      rmx = fmaxf(rmx, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rmx_l), src)));
+      bd |= __builtin_amdgcn_readlane(bad_l, src);
+    }
+    if (lane == 0) {
+      gs[grp] = rs;
+      gs[kZWaves + grp] = (double)rmn;
+      gs[2 * kZWaves + grp] = (double)rmx;
+      gs[3 * kZWaves + grp] = (double)bd;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double rsum = 0.0;
+    float rmin = __builtin_inff(), rmax = 0.f;
+    int b = 0;
+    for (int g = 0; g < rpi; g++) {
+      rsum += gs[g];
+      rmin = fminf(rmin, (float)gs[kZWaves + g]);
+      rmax = fmaxf(rmax, (float)gs[2 * kZWaves + g]);
+      b |= gs[3 * kZWaves + g] != 0.0 ? 1 : 0;
+    }
+    stg(&t.bst[band].rsum, rsum);
+    stg(&t.bst[band].ysum, ys);
+    stg(&t.bst[band].umax, um);
+    stg(&t.bst[band].rmin, rmin);
+    stg(&t.bst[band].rmax, rmax);
+    stg(&t.bst[band].bad, b);
+    stg(&t.bst[band].regime, (int32_t)regime);
+  }
+}
+
+template <int NSEG, bool MOM, bool VEC>
+__global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restrict__ TT,
+                                                        const Item *__restrict__ items, StepConsts k) {
+  __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char bufB[kZLdsBytes];
+  __shared__ float rbA[64], rbB[64];
+  __shared__ double rowsh[2 * kZRowSlots];
+  __shared__ double sh[5 * kZWaves];
+  const Item it = items[blockIdx.x];
+  const DevTensor &t = TT[it.tensor];
+  // rows per group and block: the planner keeps 4 at most with one chunk per wave, 2 with
+  // two and 1 with four, which keeps every variant's loop free of register spills
+  if (NSEG == 1 && t.zrb >= 4)
+    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+  else if (NSEG <= 2 && t.zrb >= 2)
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+  else
+    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+}
+
+// fixed-order work-group sum of p[0], p[stride], ..., p[(n-1) stride]: thread j sums
+// entries j, j + 256, ..., then a tree; every thread of the (256-thread) work-group calls it
+__device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh, int64_t stride = 1) {
+  double s = 0.0;
+  for (int64_t c = threadIdx.x; c < n; c += kThreads) s += ldg(p + c * stride);
+  return block_sum(s, sh);
+}
+// q = max(mean R, eps) for a factored tensor (the clamp of the reconstruction), from the
+// sums of R over the fold chunks of rows or over the row bands
+__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, float eps, double *sh) {
+  const double sr = t.zpath ? wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double))
+                            : wg_sum(t.rsum, t.nfr, sh);
+  return max_nan((float)(sr / (double)t.n), eps);
+}
+
+// --------------------------------------------------------------------------------------------
 // fold: R_i <- b2 R_i + a2 r_i, C_j <- b2 C_j + a2 c_j (Eq. 1), 1/sqrt(R_i), sums of R
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restrict__ TT,
@@ -273,7 +909,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     }
     const double tot = block_sum(rn, sh);
     if (threadIdx.x == 0) stg(t.rsum + it.tile, tot);
-  } else {
+  } else if (!t.zpath) {
     const int64_t j = (int64_t)(it.tile - t.nfr) * kFold + threadIdx.x;
     if (j < t.m) {
       double s = 0.0;
@@ -281,36 +917,53 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
       const float cj = (float)(s / (double)t.n);
       stg(t.C + j, fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j))));
     }
+  } else {
+    // row-band tensor: C_j, c'_j = C_j / max(mean R, eps) and sum_j z_j / c'_j over the chunk
+    const float q = mean_r_clamped(t, k.eps, sh);
+    const int64_t j = (int64_t)it.tile * kFold + threadIdx.x;
+    double sj = 0.0;
+    float cmn = __builtin_inff(), cmx = 0.f;
+    int bad = 0;
+    if (j < t.m) {
+      double cs = 0.0, zs = 0.0;
+      for (int p = 0; p < t.nzb; p++) {
+        cs += ldg(t.colpart + (int64_t)p * t.m + j);
+        zs += ldg(t.zpart + (int64_t)p * t.m + j);
+      }
+      const float cj = (float)(cs / (double)t.n);
+      const float C = fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j)));
+      stg(t.C + j, C);
+      const float cp = C / q;
+      if (C > 0.f) {
+        // c'_j that is zero or not finite leaves the tensor to the exact pass
+        if (cp > 0.f && cp < __builtin_inff()) {
+          sj = zs / (double)cp;
+          cmn = cmx = cp;
+        } else {
+          bad = 1;
+        }
+      } else if (C != 0.f || cs > 0.0 || zs > 0.0) {
+        bad = 1;   // NaN, or a nonzero column whose C underflowed
+      }
+    }
+    const double S = block_sum(sj, sh);
+    const float cmin = wg_min_wf<kWaves>(cmn, sh);
+    const float cmax = wg_max_wf<kWaves>(cmx, sh);
+    const int b = wg_or_w<kWaves>(bad, sh);
+    if (threadIdx.x == 0) {
+      stg(&t.cst[it.tile].s, S);
+      stg(&t.cst[it.tile].cmin, cmin);
+      stg(&t.cst[it.tile].cmax, cmax);
+      stg(&t.cst[it.tile].bad, b);
+    }
   }
 }
 
 // Column factors of the rank-one reconstruction: q = max(mean R, eps) and c'_j = C_j / q
 // rounded as the oracle rounds them; b_j = 1/sqrt(c'_j) in double, so that
 // 1/D_ij = min(b_j / sqrt(R_i), 1/sqrt(eps)) (Eq. 1 reconstruction with the Alg. 1 clamps).
-// fixed-order work-group sum of p[0..n): thread j sums p[j], p[j + 256], ..., then a tree;
-// every thread of the work-group must call it
-__device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh) {
-  double s = 0.0;
-  for (int64_t c = threadIdx.x; c < n; c += kThreads) s += ldg(p + c);
-  return block_sum(s, sh);
-}
-// q = max(mean R, eps) for a factored tensor (the clamp of the reconstruction)
-__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, float eps, double *sh) {
-  return max_nan((float)(wg_sum(t.rsum, t.nfr, sh) / (double)t.n), eps);
-}
 __device__ __forceinline__ double col_factor(const DevTensor &t, int64_t col, float q) {
   return 1.0 / sqrt((double)(ldg(t.C + col) / q));
-}
-
-// 8 momentum values at a 32-byte aligned position
-__device__ __forceinline__ void load_m8(const float *p, float *o) {
-  const float4 a = ldg(reinterpret_cast<const float4 *>(p));
-  const float4 b = ldg(reinterpret_cast<const float4 *>(p + 4));
-  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
-}
-__device__ __forceinline__ void store_m8(float *p, const float *v) {
-  stg(reinterpret_cast<float4 *>(p), make_float4(v[0], v[1], v[2], v[3]));
-  stg(reinterpret_cast<float4 *>(p + 4), make_float4(v[4], v[5], v[6], v[7]));
 }
 
 // --------------------------------------------------------------------------------------------
@@ -499,10 +1152,17 @@ __global__ __launch_bounds__(kThreads) void p2_exact_kernel(const DevTensor *__r
 // --------------------------------------------------------------------------------------------
 // clip stage, one work-group per tensor: k = 1 / max(1, RMS(U_hat) / d) (Sec. 3, Alg. 1),
 // NaN-propagating and rounded once to float as the oracle rounds it. With exact == 0 it
-// also records q = max(mean R, eps) and flags the tensor when the approximate sum's
-// spread (20 standard deviations, from the sum of U_hat^4) reaches a rounding boundary
-// of k or the clipping threshold; with exact == 1 it recomputes k of flagged tensors
-// from the exact sums.
+// also records q = max(mean R, eps) and flags the tensor when k's rounding is not decided
+// by the approximate sum: its spread (20 standard deviations of the free roundings)
+// reaches a rounding boundary of k or the clipping threshold. With exact == 1 it
+// recomputes k of flagged tensors from the exact pass's sums.
+//
+// Row-band tensors: when no element is on the eps floor (min R_i * min c'_j >= eps) the
+// sum is sum_j z_j / c'_j, with a spread bounded through max (s x)^2 / (R_i c'_j); when
+// every element is (max R_i * max c'_j < eps) it is the exactly rounded floored sum.
+// Otherwise both are upper bounds of the oracle's sum (an element's U_hat^2 is at most
+// its unfloored and its floored value, up to rounding); below the clipping threshold k
+// is exactly 1, and above it the tensor goes to the exact pass.
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restrict__ TT,
                                                         const Item *__restrict__ items, StepConsts k, int exact) {
@@ -511,23 +1171,80 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   const DevTensor &t = TT[it.tensor];
   if (exact && ldg(&t.sc->ambiguous) == 0) return;
   const int64_t ntiles = (int64_t)t.ntr * t.ntc;
-  const double S = wg_sum(t.ssum, ntiles, sh);
-  const double Q4 = exact ? 0.0 : wg_sum(t.qsum, ntiles, sh);
-  const float q = (!exact && t.kind == kFactored) ? mean_r_clamped(t, k.eps, sh) : 0.f;
-  if (threadIdx.x != 0) return;
-  const double r = sqrt(S / (double)(t.n * t.m)) / (double)k.d;
-  const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
-  const double kd = 1.0 / den;
-  const float kf = (float)kd;
+  const double N = (double)(t.n * t.m);
   if (exact) {
-    stg(&t.sc->k, kf);
+    const double S = wg_sum(t.ssum, ntiles, sh);
+    if (threadIdx.x != 0) return;
+    const double r = sqrt(S / N) / (double)k.d;
+    const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
+    stg(&t.sc->k, (float)(1.0 / den));
     stg(&t.sc->ambiguous, 2);
     return;
   }
+  const float q = t.kind == kFactored ? mean_r_clamped(t, k.eps, sh) : 0.f;
+  double S = 0.0, spread = 0.0;
   bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t.kind == kFactored;
-  if (S > 0.0 && r == r && r < 1e300) {
-    const double spread = 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14;   // relative, on S
-    if (fabs(r - 1.0) <= spread) amb = true;                         // at the clipping threshold
+  if (t.zpath) {
+    const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
+    const double Y = wg_sum(&t.bst->ysum, t.nzb, sh, bstride);
+    const double SU = wg_sum(&t.cst->s, t.nfc, sh, cstride);
+    double um = 0.0;
+    float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
+    int bad = 0;
+    for (int64_t b = threadIdx.x; b < t.nzb; b += kThreads) {
+      um = fmax(um, ldg(&t.bst[b].umax));
+      rmn = fminf(rmn, ldg(&t.bst[b].rmin));
+      rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
+      bad |= ldg(&t.bst[b].bad);
+    }
+    for (int64_t c = threadIdx.x; c < t.nfc; c += kThreads) {
+      cmn = fminf(cmn, ldg(&t.cst[c].cmin));
+      cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
+      bad |= ldg(&t.cst[c].bad);
+    }
+    um = wg_max_w<kWaves>(um, sh);
+    rmn = wg_min_wf<kWaves>(rmn, sh);
+    rmx = wg_max_wf<kWaves>(rmx, sh);
+    cmn = wg_min_wf<kWaves>(cmn, sh);
+    cmx = wg_max_wf<kWaves>(cmx, sh);
+    bad = wg_or_w<kWaves>(bad, sh);
+    if (threadIdx.x != 0) return;
+    // the sums the row-band pass formed this step (it skips one when the last step predicts
+    // the regime); a sum it did not form counts as +inf
+    const int formed = ldg(&t.bst[0].regime);
+    const bool have_z = formed != kRegimeFloor, have_y = formed != kRegimeAbove;
+    const double inf = __builtin_inf();
+    const double SUf = have_z ? SU : inf, Yf = have_y ? Y : inf;
+    const bool finite = !(SUf != SUf) && !(Yf != Yf) && (SUf < 1e300 || Yf < 1e300);
+    const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
+    if (bad || !finite) {
+      amb = true;
+      S = SU;
+    } else if (have_z && lo >= k.eps) {   // nothing on the floor
+      S = SU;
+      spread = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) / SU + 1e-14 : 0.0;
+    } else if (have_y && hi < k.eps) {    // everything on the floor
+      S = Y;
+      spread = 1e-14;
+    } else {
+      S = fmin(SUf, Yf) * (1.0 + 1e-6);   // an upper bound of the oracle's sum
+      if (!(sqrt(S / N) / (double)k.d < 1.0)) amb = true;
+    }
+    // the next step's prediction, with a factor-2 margin on either side of the floor
+    const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
+    stg(&t.sc->regime, (bad || !finite) ? (int32_t)kRegimeBoth : (int32_t)next);
+  } else {
+    S = wg_sum(t.ssum, ntiles, sh);
+    const double Q4 = wg_sum(t.qsum, ntiles, sh);
+    if (threadIdx.x != 0) return;
+    spread = 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14;   // relative, on S
+  }
+  const double r = sqrt(S / N) / (double)k.d;
+  const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
+  const double kd = 1.0 / den;
+  const float kf = (float)kd;
+  if (!amb && S > 0.0 && r == r && r < 1e300 && spread > 0.0) {
+    if (fabs(r - 1.0) <= spread) amb = true;   // at the clipping threshold
     if (r > 1.0) {
       const double up = (double)nextafterf(kf, 3.0e38f), dn = (double)nextafterf(kf, 0.f);
       const double mid_hi = 0.5 * ((double)kf + up), mid_lo = 0.5 * ((double)kf + dn);
@@ -722,6 +1439,30 @@ __global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restric
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(p1_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items);
+  return (int)hipGetLastError();
+}
+int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, void *stream) {
+  if (count <= 0) return hipSuccess;
+  const dim3 grid((uint32_t)count), block(kZThreads);
+  hipStream_t s = (hipStream_t)stream;
+  switch (variant) {
+#define SKEW_P1Z_CASE(V, NSEG, VEC, MOM) \
+  case V: hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC>), grid, block, 0, s, T, items, k); break;
+    SKEW_P1Z_CASE(0, 1, true, false)
+    SKEW_P1Z_CASE(1, 1, true, true)
+    SKEW_P1Z_CASE(2, 1, false, false)
+    SKEW_P1Z_CASE(3, 1, false, true)
+    SKEW_P1Z_CASE(4, 2, true, false)
+    SKEW_P1Z_CASE(5, 2, true, true)
+    SKEW_P1Z_CASE(6, 2, false, false)
+    SKEW_P1Z_CASE(7, 2, false, true)
+    SKEW_P1Z_CASE(8, 4, true, false)
+    SKEW_P1Z_CASE(9, 4, true, true)
+    SKEW_P1Z_CASE(10, 4, false, false)
+    SKEW_P1Z_CASE(11, 4, false, true)
+#undef SKEW_P1Z_CASE
+    default: return (int)hipErrorInvalidValue;
+  }
   return (int)hipGetLastError();
 }
 int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {

@@ -1,6 +1,6 @@
 // skew_plan.cpp -- host-only planning of a descriptor table: validation, the tier
 // state each tensor keeps (Fig. 1; Sec. 3 "The tiers"), the state size of Eq. 2
-// (plus the exact v of vectors, Table 6), the tile grid and the work-item lists.
+// (plus the exact v of vectors, Table 6), the tile grids and the work-item lists.
 // No HIP calls: this runs without a GPU.
 #include <algorithm>
 #include <climits>
@@ -69,7 +69,39 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
     tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
     p.clip.push_back({i, 0});
-    if (tp.kind == kFactored) {
+    // Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
+    // row, nseg (1, 2 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
+    // row and zrpi = 8 / wpr rows are side by side. A block of zrpi * zrb rows (bf16
+    // gradient, plus fp32 momentum on the backbone) fills at most one LDS buffer.
+    const int64_t zcw = ceil_div(tp.m, kChunk);
+    const int64_t nseg = zcw <= 1 ? 1 : (zcw <= 2 * kZWaves ? 2 : 4);
+    const int64_t wpr = ceil_div(zcw, nseg);
+    const int64_t row_kb = zcw * (tp.momentum ? 3 : 1);   // staged KiB per row
+    const int64_t rpi = wpr <= kZWaves ? kZWaves / wpr : 0;
+    int64_t zrb = rpi > 0 ? std::min<int64_t>(4 / nseg, kZLdsBytes / (rpi * row_kb * 1024)) : 0;
+    while (zrb & (zrb - 1)) zrb &= zrb - 1;   // a power of two: 1, 2 or 4
+    tp.zpath = (tp.kind == kFactored && rpi > 0 && zrb >= 1) ? 1 : 0;
+    if (tp.zpath) {
+      tp.zcw = (int32_t)zcw;
+      tp.nseg = (int32_t)nseg;
+      tp.zrpi = (int32_t)rpi;
+      tp.zrb = (int32_t)zrb;
+      const int64_t rows_block = rpi * zrb;
+      tp.zrows = ceil_div(std::max<int64_t>(1, ceil_div(kZBandElems, tp.m)), rows_block) * rows_block;
+      const int64_t nzb = ceil_div(tp.n, tp.zrows), nfc = ceil_div(tp.m, kFold);
+      if (nzb > INT32_MAX / 2 || nfc > INT32_MAX / 2) return SKEW_EINVAL;
+      tp.nzb = (int32_t)nzb;
+      tp.nfr = 0;
+      tp.nfc = (int32_t)nfc;
+      tp.off_colpart = ws_part; ws_part = align_up(ws_part + (size_t)nzb * tp.m * 8);
+      tp.off_zpart = ws_part; ws_part = align_up(ws_part + (size_t)nzb * tp.m * 8);
+      tp.off_ainv = ws_part; ws_part = align_up(ws_part + (size_t)tp.n * 8);
+      tp.off_bst = ws_part; ws_part = align_up(ws_part + (size_t)nzb * sizeof(BandStats));
+      tp.off_cst = ws_part; ws_part = align_up(ws_part + (size_t)nfc * sizeof(ColStats));
+      for (int32_t k = 0; k < tp.nzb; k++) p.z.push_back({i, k});
+      for (int32_t k = 0; k < tp.nfc; k++) p.fold.push_back({i, k});
+      items_total += nzb + nfc;
+    } else if (tp.kind == kFactored) {
       const int64_t nfr = ceil_div(tp.n, kFold), nfc = ceil_div(tp.m, kFold);
       if (nfr + nfc > INT32_MAX / 2) return SKEW_EINVAL;
       tp.nfr = (int32_t)nfr;
@@ -82,28 +114,29 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold.push_back({i, k});
       items_total += tiles + nfr + nfc;
     }
-    for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p2.push_back({i, k});
+    if (!tp.zpath) {
+      for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p2.push_back({i, k});
+      items_total += tiles;
+    }
     for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p3.push_back({i, k});
-    items_total += 2 * tiles;
+    items_total += tiles;
     if (items_total > INT32_MAX / 2) return SKEW_EINVAL;
   }
   p.state_bytes = st;
-  // workspace: [device tensor table][items p1|fold|p2|p3][partials]
+  // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][partials]
   size_t ws = 0;
   p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
   p.off_items = ws;
-  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1));
+  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
+                                     p.clip.size() + 1));
+  auto shift = [ws](size_t &off) {
+    if (off != SIZE_MAX) off += ws;
+  };
   for (auto &tp : p.t) {
     if (tp.empty) continue;
-    tp.off_ssum += ws;
-    tp.off_qsum += ws;
-    tp.off_sc += ws;
-    if (tp.kind == kFactored) {
-      tp.off_rowpart += ws;
-      tp.off_colpart += ws;
-      tp.off_ainv += ws;
-      tp.off_rsum += ws;
-    }
+    for (size_t *o : {&tp.off_ssum, &tp.off_qsum, &tp.off_sc, &tp.off_rowpart, &tp.off_colpart, &tp.off_ainv,
+                      &tp.off_rsum, &tp.off_zpart, &tp.off_bst, &tp.off_cst})
+      shift(*o);
   }
   p.ws_bytes = ws + ws_part;
   *out = std::move(p);

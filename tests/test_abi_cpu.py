@@ -58,7 +58,7 @@ def test_state_bytes_match_closed_form(name):
     assert wb > 0
     if name == "full":
         assert closed == 1_384_279_040          # 1.289 GiB for the 6.78B synthetic set
-        assert wb < 0.02 * 12.64 * 2**30        # partial sums stay a small fraction of G
+        assert wb < 0.03 * 12.64 * 2**30        # partial sums stay a small fraction of G
 
 
 def test_paper_inventory_state_bytes():

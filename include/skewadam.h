@@ -124,8 +124,8 @@ int skew_state_bytes(const skew_tensor_desc *d, int n, size_t *state_bytes, size
  *               state: saving it with the step counter and seed is a checkpoint, and
  *               copying it back after a new skew_state_init() on an identical table
  *               resumes bit-exactly.
- *   workspace   device buffer of >= workspace_bytes; the library owns its contents
- *               until skew_destroy().
+ *   workspace   device buffer of >= workspace_bytes; zero-filled on `stream`; the library
+ *               owns its contents until skew_destroy().
  *   stream      hipStream_t as void*.
  * All pointers must stay valid and unchanged until skew_destroy(); to change them,
  * destroy and init again. Errors: SKEW_EINVAL, SKEW_ENOSPACE, SKEW_ENOMEM, SKEW_EHIP. */
@@ -137,6 +137,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
  * synchronisation). Reads g, updates w and the state in place. One step per
  * context may be in flight at a time. Non-finite gradients propagate into the
  * state and weights (a NaN makes the clip factor NaN, so its whole tensor).
+ * The state's and workspace's contents between steps belong to the library.
  * Errors: SKEW_EINVAL (ctx NULL, hp invalid), SKEW_EHIP (launch failed). */
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream);
 
@@ -162,6 +163,22 @@ int skew_abi_version(void);
 int skew_timing_enable(skew_ctx *ctx, int max_steps);
 int skew_timing_read(skew_ctx *ctx, double *ms, int max_launches, int *launches, int *steps);
 const char *skew_launch_name(skew_ctx *ctx, int j);
+
+/* ---- Diagnostics: how the last step decided each tensor's clip factor ----
+ * skew_clip_info(ctx, k, route, n, stream) waits for `stream`, then for every tensor i of
+ * the table (n >= table size; host arrays of n entries) writes
+ *   k[i]      the clip factor the last step applied (Sec. 3 "Update clipping"),
+ *   route[i]  bits 0..3: how k was decided: 0 from the fast sums, 4 by the re-check that
+ *             tests each element against the eps floor, 2 by the re-check that follows
+ *             the reference float sequence;
+ *             bits 4..7 (with 2 or 4): why a re-check ran: 1 forced by
+ *             SKEW_FLAG_EXACT_CLIP, 2 non-finite values, 3 elements on both sides of the
+ *             eps floor, 4 the floor regime changed from the one predicted, 5 a sum's
+ *             error bound reaches a rounding boundary of k or the clipping threshold;
+ *             bits 8..15: the sums the next step's row-band pass will form
+ *             (0 both, 1 only the one above the eps floor, 2 only the floored one).
+ * Empty tensors report k = 0, route = 0. Errors: SKEW_EINVAL, SKEW_EHIP. */
+int skew_clip_info(skew_ctx *ctx, float *k, int32_t *route, int n, void *stream);
 
 #ifdef __cplusplus
 }

@@ -1,6 +1,7 @@
 // skew_api.cpp -- the C ABI declared in include/skewadam.h.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -18,17 +19,36 @@ const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_s
                                              "p2_exact_recheck", "clip_factor_recheck", "p3_apply_dither"};
 }  // namespace
 
+// an item list with the bounds of each pipeline group in it
+struct GroupedList {
+  Item *d = nullptr;
+  std::vector<int64_t> bound;   // group g: items [bound[g], bound[g + 1])
+  int64_t count(int g) const { return bound[g + 1] - bound[g]; }
+  const Item *at(int g) const { return d + bound[g]; }
+};
+
 struct skew_ctx {
   Plan plan;
+  char *ws = nullptr;   // workspace base (device)
   DevTensor *d_table = nullptr;
-  Item *d_p1 = nullptr, *d_fold = nullptr, *d_p2 = nullptr, *d_p3 = nullptr, *d_clip = nullptr;
-  Item *d_z[kZVariants] = {};     // row-band pass items, one list per kernel variant
-  int64_t n_z[kZVariants] = {};
-  // diagnostics: events [step][kLaunches + 1]
-  std::vector<hipEvent_t> ev;
+  RecheckLists *lists = nullptr;
+  GroupedList p1, fold, p2, p3, clip;
+  GroupedList z[kZVariants];   // row-band pass items, one list per kernel variant
+  hipStream_t side = nullptr;  // the update pass of the pipeline runs here
+  std::vector<hipEvent_t> sync;   // [0]: step start, [1]: update pass done, [2 + g]: group g ready
+  // diagnostics: per recorded step, (launch kind, start event, end event) of every launch
+  struct Timed {
+    int kind;
+    hipEvent_t a, b;
+  };
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::vector<Timed>> timed;
   int ev_steps = 0, ev_used = 0;
+  size_t ev_next = 0;
   ~skew_ctx() {
-    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+    for (hipEvent_t e : sync) (void)hipEventDestroy(e);
+    if (side) (void)hipStreamDestroy(side);
   }
 };
 
@@ -159,42 +179,46 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.tensor_id = d[i].tensor_id;
   }
   // row-band pass items by kernel variant (16-byte aligned rows or element loads is known
-  // only here, from the pointers)
+  // only here, from the pointers); every list keeps tensor order, so each pipeline group
+  // is a contiguous range of it
   std::vector<Item> zv[kZVariants];
   for (const Item &it : p.z) {
     const DevTensor &x = table[it.tensor];
     const int lg = x.nseg == 1 ? 0 : (x.nseg == 2 ? 1 : 2);
     zv[lg * 4 + (x.vec ? 0 : 2) + (x.momentum ? 1 : 0)].push_back(it);
   }
-  std::vector<Item> items;
-  items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
-  items.insert(items.end(), p.p1.begin(), p.p1.end());
-  for (const auto &v : zv) items.insert(items.end(), v.begin(), v.end());
-  items.insert(items.end(), p.fold.begin(), p.fold.end());
-  items.insert(items.end(), p.p2.begin(), p.p2.end());
-  items.insert(items.end(), p.p3.begin(), p.p3.end());
-  items.insert(items.end(), p.clip.begin(), p.clip.end());
-  if (items.empty()) items.push_back({0, 0});
-
   skew_ctx *c = new (std::nothrow) skew_ctx;
   if (c == nullptr) return SKEW_ENOMEM;
   c->d_table = reinterpret_cast<DevTensor *>(ws + p.off_table);
-  Item *base = reinterpret_cast<Item *>(ws + p.off_items);
-  c->d_p1 = base;
-  Item *cur = c->d_p1 + p.p1.size();
-  for (int v = 0; v < kZVariants; v++) {
-    c->d_z[v] = cur;
-    c->n_z[v] = (int64_t)zv[v].size();
-    cur += zv[v].size();
-  }
-  c->d_fold = cur;
-  c->d_p2 = c->d_fold + p.fold.size();
-  c->d_p3 = c->d_p2 + p.p2.size();
-  c->d_clip = c->d_p3 + p.p3.size();
+  c->lists = reinterpret_cast<RecheckLists *>(ws + p.off_lists);
+  Item *const base = reinterpret_cast<Item *>(ws + p.off_items);
+  std::vector<Item> items;
+  items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
+  auto add = [&](GroupedList &gl, const std::vector<Item> &v) {
+    gl.d = base + items.size();
+    gl.bound.assign((size_t)p.ngroups + 1, 0);
+    for (const Item &it : v) gl.bound[(size_t)p.tgroup[it.tensor] + 1]++;
+    for (int g = 0; g < p.ngroups; g++) gl.bound[g + 1] += gl.bound[g];
+    items.insert(items.end(), v.begin(), v.end());
+  };
+  add(c->p1, p.p1);
+  for (int v = 0; v < kZVariants; v++) add(c->z[v], zv[v]);
+  add(c->fold, p.fold);
+  add(c->p2, p.p2);
+  add(c->p3, p.p3);
+  add(c->clip, p.clip);
+  if (items.empty()) items.push_back({0, 0});
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = hipSuccess;
-  if (p.state_bytes > 0) e = hipMemsetAsync(state, 0, p.state_bytes, s);
+  hipError_t e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+  for (int i = 0; e == hipSuccess && i < p.ngroups + 2; i++) {
+    hipEvent_t ev;
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e == hipSuccess) c->sync.push_back(ev);
+  }
+  // zero state and workspace (the per-tensor scalars start with no regime prediction)
+  if (e == hipSuccess && p.state_bytes > 0) e = hipMemsetAsync(state, 0, p.state_bytes, s);
+  if (e == hipSuccess) e = hipMemsetAsync(ws, 0, p.ws_bytes, s);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->d_table, table.data(), sizeof(DevTensor) * table.size(), hipMemcpyHostToDevice, s);
   if (e == hipSuccess)
@@ -205,6 +229,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     return SKEW_EHIP;
   }
   c->plan = std::move(p);
+  c->ws = ws;
   *ctx = c;
   return SKEW_OK;
 }
@@ -213,50 +238,91 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
   const StepConsts k = make_consts(*hp);
   const Plan &p = ctx->plan;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  hipEvent_t *ev = nullptr;
-  if (ctx->ev_used < ctx->ev_steps) ev = &ctx->ev[(size_t)ctx->ev_used++ * (kLaunches + 1)];
-  int e = ev ? (int)hipEventRecord(ev[0], s) : 0;
-  // launch j of the step, then (with timing on) the event that ends it
-  auto run = [&](int j, int rc) {
-    if (e == 0) e = rc;
-    if (e == 0 && ev) e = (int)hipEventRecord(ev[j + 1], s);
+  hipStream_t s0 = static_cast<hipStream_t>(stream), s1 = ctx->side;
+  std::vector<skew_ctx::Timed> *rec = nullptr;
+  if (ctx->ev_used < ctx->ev_steps) {
+    rec = &ctx->timed[(size_t)ctx->ev_used++];
+    rec->clear();
+  }
+  int e = 0;
+  // one launch of kind j on stream st, bracketed by timing events when recording
+  auto run = [&](int j, hipStream_t st, auto &&launch) {
+    if (e != 0) return;
+    if (rec && ctx->ev_next + 2 <= ctx->ev_pool.size()) {
+      skew_ctx::Timed t{j, ctx->ev_pool[ctx->ev_next], ctx->ev_pool[ctx->ev_next + 1]};
+      ctx->ev_next += 2;
+      e = (int)hipEventRecord(t.a, st);
+      if (e == 0) e = launch();
+      if (e == 0) e = (int)hipEventRecord(t.b, st);
+      rec->push_back(t);
+    } else {
+      e = launch();
+    }
   };
   const DevTensor *T = ctx->d_table;
-  // row-band pass: the main variant (aligned rows, no momentum) is launch 0, the rest launch 1
-  if (e == 0) run(0, launch_p1z(T, ctx->d_z[0], ctx->n_z[0], k, 0, stream));
-  if (e == 0) {
-    int rc = 0;
-    for (int v = 1; v < kZVariants && rc == 0; v++) rc = launch_p1z(T, ctx->d_z[v], ctx->n_z[v], k, v, stream);
-    run(1, rc);
+  // the side stream starts after everything the caller queued before the step
+  if (p.ngroups > 1) {
+    e = (int)hipEventRecord(ctx->sync[0], s0);
+    if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[0], 0);
   }
-  if (e == 0) run(2, launch_p1(T, ctx->d_p1, (int64_t)p.p1.size(), stream));
-  if (e == 0) run(3, launch_fold(T, ctx->d_fold, (int64_t)p.fold.size(), k, stream));
-  if (e == 0) run(4, launch_p2(T, ctx->d_p2, (int64_t)p.p2.size(), k, stream));
-  if (e == 0) run(5, launch_clip(T, ctx->d_clip, (int64_t)p.clip.size(), k, 0, stream));
-  // the exact re-check runs over every tile; tensors the clip stage did not flag exit at once
-  if (e == 0) run(6, launch_p2_exact(T, ctx->d_p3, (int64_t)p.p3.size(), k, stream));
-  if (e == 0) run(7, launch_clip(T, ctx->d_clip, (int64_t)p.clip.size(), k, 1, stream));
-  if (e == 0) run(8, launch_p3(T, ctx->d_p3, (int64_t)p.p3.size(), k, stream));
+  for (int g = 0; g < p.ngroups && e == 0; g++) {
+    // pass 1, fold and clip stage of group g on the caller's stream
+    for (int v = 0; v < kZVariants; v++)
+      if (ctx->z[v].count(g) > 0)
+        run(v == 0 ? 0 : 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, s0); });
+    if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
+    if (ctx->fold.count(g) > 0) run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, s0); });
+    if (ctx->p2.count(g) > 0) run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
+    if (ctx->clip.count(g) > 0) {
+      const int nt = (int)p.t.size();
+      RecheckLists *L = ctx->lists;
+      run(5, s0, [&] { return launch_clip(T, ctx->clip.at(g), ctx->clip.count(g), k, L, nt, s0); });
+      // re-checks of the tensors the clip stage listed (launches with empty lists exit at once)
+      run(6, s0, [&] { return launch_recheck(T, L, nt, k, 1, s0); });
+      run(7, s0, [&] { return launch_clip_recheck(T, L, nt, k, 1, s0); });
+      run(6, s0, [&] { return launch_recheck(T, L, nt, k, 2, s0); });
+      run(7, s0, [&] { return launch_clip_recheck(T, L, nt, k, 2, s0); });
+    }
+    if (p.ngroups == 1) {
+      if (ctx->p3.count(g) > 0)
+        run(8, s0, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, ctx->lists, s0); });
+      continue;
+    }
+    if (e == 0) e = (int)hipEventRecord(ctx->sync[2 + g], s0);
+    // the update pass of group g on the side stream, concurrent with pass 1 of group g + 1
+    if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[2 + g], 0);
+    if (ctx->p3.count(g) > 0)
+      run(8, s1, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, ctx->lists, s1); });
+  }
+  // the caller's stream continues after the last update
+  if (e == 0 && p.ngroups > 1) {
+    e = (int)hipEventRecord(ctx->sync[1], s1);
+    if (e == 0) e = (int)hipStreamWaitEvent(s0, ctx->sync[1], 0);
+  }
   return e == 0 ? SKEW_OK : SKEW_EHIP;
 }
 
 int skew_timing_enable(skew_ctx *ctx, int max_steps) {
   if (ctx == nullptr || max_steps < 0) return SKEW_EINVAL;
-  for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
-  ctx->ev.clear();
+  for (hipEvent_t e : ctx->ev_pool) (void)hipEventDestroy(e);
+  ctx->ev_pool.clear();
+  ctx->timed.clear();
   ctx->ev_steps = ctx->ev_used = 0;
-  const size_t n = (size_t)max_steps * (kLaunches + 1);
-  ctx->ev.reserve(n);
+  ctx->ev_next = 0;
+  // at most one launch of each kind per group and step (the row-band variants share two kinds)
+  const size_t per_step = (size_t)ctx->plan.ngroups * (kLaunches + kZVariants + 2) * 2;
+  const size_t n = (size_t)max_steps * per_step;
+  ctx->ev_pool.reserve(n);
   for (size_t i = 0; i < n; i++) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) {
-      for (hipEvent_t x : ctx->ev) (void)hipEventDestroy(x);
-      ctx->ev.clear();
+      for (hipEvent_t x : ctx->ev_pool) (void)hipEventDestroy(x);
+      ctx->ev_pool.clear();
       return SKEW_EHIP;
     }
-    ctx->ev.push_back(e);
+    ctx->ev_pool.push_back(e);
   }
+  ctx->timed.resize((size_t)max_steps);
   ctx->ev_steps = max_steps;
   return SKEW_OK;
 }
@@ -265,23 +331,45 @@ int skew_timing_read(skew_ctx *ctx, double *ms, int max_launches, int *launches,
   if (ctx == nullptr || ms == nullptr || max_launches < kLaunches) return SKEW_EINVAL;
   for (int j = 0; j < kLaunches; j++) ms[j] = 0.0;
   for (int st = 0; st < ctx->ev_used; st++) {
-    hipEvent_t *ev = &ctx->ev[(size_t)st * (kLaunches + 1)];
-    if (hipEventSynchronize(ev[kLaunches]) != hipSuccess) return SKEW_EHIP;
-    for (int j = 0; j < kLaunches; j++) {
-      float t = 0.f;
-      if (hipEventElapsedTime(&t, ev[j], ev[j + 1]) != hipSuccess) return SKEW_EHIP;
-      ms[j] += t;
+    for (const skew_ctx::Timed &t : ctx->timed[(size_t)st]) {
+      float ms1 = 0.f;
+      if (hipEventSynchronize(t.b) != hipSuccess || hipEventElapsedTime(&ms1, t.a, t.b) != hipSuccess)
+        return SKEW_EHIP;
+      ms[t.kind] += ms1;
     }
   }
   if (launches) *launches = kLaunches;
   if (steps) *steps = ctx->ev_used;
   ctx->ev_used = 0;
+  ctx->ev_next = 0;
   return SKEW_OK;
 }
 
 const char *skew_launch_name(skew_ctx *ctx, int j) {
   (void)ctx;
   return (j >= 0 && j < kLaunches) ? kLaunchNames[j] : "";
+}
+
+int skew_clip_info(skew_ctx *ctx, float *k, int32_t *route, int n, void *stream) {
+  if (ctx == nullptr || k == nullptr || route == nullptr || n < (int)ctx->plan.t.size()) return SKEW_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nt = (int)ctx->plan.t.size();
+  std::vector<TensorScalars> sc((size_t)std::max(nt, 1));
+  for (int i = 0; i < nt; i++) {
+    const TensorPlan &tp = ctx->plan.t[i];
+    if (tp.empty) {
+      std::memset(&sc[i], 0, sizeof(TensorScalars));
+      continue;
+    }
+    if (hipMemcpyAsync(&sc[i], ctx->ws + tp.off_sc, sizeof(TensorScalars), hipMemcpyDeviceToHost, s) != hipSuccess)
+      return SKEW_EHIP;
+  }
+  if (hipStreamSynchronize(s) != hipSuccess) return SKEW_EHIP;
+  for (int i = 0; i < nt; i++) {
+    k[i] = sc[i].k;
+    route[i] = (sc[i].ambiguous & 0xFF) | ((ctx->plan.t[i].zpath ? sc[i].regime & 0xFF : 0) << 8);
+  }
+  return SKEW_OK;
 }
 
 void skew_destroy(skew_ctx *ctx) { delete ctx; }

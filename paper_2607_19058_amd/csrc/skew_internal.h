@@ -32,9 +32,36 @@ constexpr int kZMaxBlockRows = 64;       // rows staged per block, at most
 struct TensorScalars {
   float k;            // clip factor 1 / max(1, RMS(U_hat) / d), rounded as the oracle rounds it
   float q;            // max(mean R, eps) (factored tensors)
-  int32_t ambiguous;  // 1: the approximate sum left k's rounding undecided; the exact pass decides
+  int32_t ambiguous;  // bits 0..3: kClip* (how k was decided); bits 4..7: why a re-check ran (kWhy*)
   int32_t regime;     // row-band tensors, set by the clip stage for the next step: which sums the
                       // row-band pass forms (kRegime*); zero (both) after skew_state_init
+};
+// Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
+// launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for
+// the exact float sequence. Counts are zeroed by the update pass at the end of each step.
+struct RecheckLists {
+  int32_t n1, n2;
+  int32_t pad[62];
+  // followed by int32 l1[ntensors], int32 l2[ntensors]
+};
+constexpr int kRecheckGrid = 1024;   // work-groups of a re-check launch
+
+// States of TensorScalars::ambiguous (bits 0..3)
+enum ClipState : int32_t {
+  kClipFast = 0,        // decided from the fast sums
+  kClipPending1 = 1,    // listed for the re-check with the exact floor split
+  kClipExact = 2,       // decided by the exact float sequence
+  kClipPending2 = 3,    // listed for the exact float sequence
+  kClipSplit = 4        // decided by the re-check with the exact floor split
+};
+
+// Why the clip stage sent a tensor to the exact pass.
+enum Why : int32_t {
+  kWhyForced = 1,       // SKEW_FLAG_EXACT_CLIP
+  kWhyNonFinite = 2,    // a non-finite sum or statistic
+  kWhyStraddle = 3,     // elements on both sides of the eps floor, and the bound reaches the threshold
+  kWhyMissingSum = 4,   // the regime changed from the prediction, and the bound reaches the threshold
+  kWhySpread = 5        // the fast sum's spread reaches a rounding boundary of k or the threshold
 };
 // Which update sums the row-band pass forms: both, only the one above the eps floor
 // (the last step had every element clearly above it), or only the floored one.
@@ -126,10 +153,20 @@ struct TensorPlan {
   int64_t zrows = 0;
 };
 
+// The step can run as a two-stream pipeline over groups of consecutive tensors (about
+// equal algorithmic bytes): the update pass (p3) of group g on one stream while pass 1,
+// the fold and the clip stage of group g + 1 run on the other. Measured on the 6.78B
+// workload, the two passes slow each other down more than they overlap (the row-band
+// pass needs whole CUs), so one group is used: every launch covers all tensors.
+constexpr int kMaxGroups = 1;
+
 struct Plan {
   std::vector<TensorPlan> t;
+  size_t off_lists = 0;                       // workspace offset of the RecheckLists
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
   std::vector<Item> z;                        // row-band pass items (split by kernel variant at init)
+  int32_t ngroups = 1;
+  std::vector<int32_t> tgroup;                // group of each tensor (item lists are in tensor order)
   size_t state_bytes = 0;
   size_t ws_bytes = 0;
   size_t off_table = 0, off_items = 0;   // workspace offsets of the device table and item lists
@@ -147,8 +184,14 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
 
 int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
-int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
-int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int exact, void *stream);
-int launch_p2_exact(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
+              void *stream);
+int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
+                int ntensors, void *stream);
+// re-check of the listed tensors: level 1 (exact floor split) or 2 (exact float sequence),
+// then their clip factors from the new sums
+int launch_recheck(const DevTensor *T, RecheckLists *L, int ntensors, const StepConsts &k, int level, void *stream);
+int launch_clip_recheck(const DevTensor *T, RecheckLists *L, int ntensors, const StepConsts &k, int level,
+                        void *stream);
 
 }  // namespace skew

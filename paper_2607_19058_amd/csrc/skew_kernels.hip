@@ -1136,17 +1136,99 @@ __global__ __launch_bounds__(kThreads) void p2_kernel(const DevTensor *__restric
   }
 }
 
-// exact re-run of p2 for the tensors the clip stage left undecided (others exit at once)
-__global__ __launch_bounds__(kThreads) void p2_exact_kernel(const DevTensor *__restrict__ TT,
-                                                            const Item *__restrict__ items, StepConsts k) {
+// Re-check of the listed tensors over their tiles: level 1 forms the update sum with the
+// exact floor test per element (the floored part exactly rounded, the rest unrounded, and
+// the sum of U_hat^4 over the rest for its spread); level 2 follows the oracle's float
+// sequence exactly. A fixed grid walks the (tensor, tile) pairs of the list.
+__device__ __forceinline__ int32_t *recheck_list(RecheckLists *L, int ntensors, int level) {
+  int32_t *l1 = reinterpret_cast<int32_t *>(L + 1);
+  return level == 1 ? l1 : l1 + ntensors;
+}
+
+__global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__restrict__ TT, RecheckLists *L,
+                                                           int ntensors, StepConsts k, int level) {
   __shared__ double sh[kThreads];
-  const Item it = items[blockIdx.x];
-  const DevTensor &t = TT[it.tensor];
-  if (t.kind != kFactored || ldg(&t.sc->ambiguous) == 0) return;
-  const Tile tl = tile_of(t, it.tile);
-  const float q = mean_r_clamped(t, k.eps, sh);
-  const double s = block_sum(p2_factored_exact(t, tl, k, q), sh);
-  if (threadIdx.x == 0) stg(t.ssum + it.tile, s);
+  const int n = ldg(level == 1 ? &L->n1 : &L->n2);
+  if (n <= 0) return;
+  const int32_t *list = recheck_list(L, ntensors, level);
+  int64_t total = 0;
+  for (int j = 0; j < n; j++) {
+    const DevTensor &t = TT[ldg(list + j)];
+    total += (int64_t)t.ntr * t.ntc;
+  }
+  for (int64_t idx = blockIdx.x; idx < total; idx += gridDim.x) {
+    int64_t base = 0;
+    int j = 0;
+    for (;; j++) {
+      const DevTensor &t = TT[ldg(list + j)];
+      const int64_t nt = (int64_t)t.ntr * t.ntc;
+      if (idx < base + nt) break;
+      base += nt;
+    }
+    const DevTensor &t = TT[ldg(list + j)];
+    const int tile = (int)(idx - base);
+    const Tile tl = tile_of(t, tile);
+    const float q = mean_r_clamped(t, k.eps, sh);
+    if (level == 1) {
+      const SumPair acc = p2_factored(t, tl, k, q);
+      const double sv = block_sum(acc.s, sh);
+      const double q4 = block_sum(acc.q4, sh);
+      if (threadIdx.x == 0) {
+        stg(t.ssum + tile, sv);
+        stg(t.qsum + tile, q4);
+      }
+    } else {
+      const double sv = block_sum(p2_factored_exact(t, tl, k, q), sh);
+      if (threadIdx.x == 0) stg(t.ssum + tile, sv);
+    }
+  }
+}
+
+// k = 1 / max(1, RMS / d) from the sum S over N elements, rounded once to float (NaN
+// propagates); `amb` when a relative spread of S may move k across a rounding boundary of
+// the float or across the clipping threshold
+__device__ __forceinline__ float clip_from_sum(double S, double N, float d, double spread, bool &amb) {
+  const double r = sqrt(S / N) / (double)d;
+  const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
+  const double kd = 1.0 / den;
+  const float kf = (float)kd;
+  if (!amb && S > 0.0 && r == r && r < 1e300 && spread > 0.0) {
+    if (fabs(r - 1.0) <= spread) amb = true;   // at the clipping threshold
+    if (r > 1.0) {
+      const double up = (double)nextafterf(kf, 3.0e38f), dn = (double)nextafterf(kf, 0.f);
+      const double mid_hi = 0.5 * ((double)kf + up), mid_lo = 0.5 * ((double)kf + dn);
+      const double tol = 0.5 * spread * kd;
+      if (fabs(kd - mid_hi) <= tol || fabs(kd - mid_lo) <= tol) amb = true;
+    }
+  }
+  return kf;
+}
+
+// clip factors of the listed tensors from the re-check's sums; level 1 lists for level 2
+// the tensors whose spread still leaves k undecided
+__global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor *__restrict__ TT, RecheckLists *L,
+                                                                int ntensors, StepConsts k, int level) {
+  __shared__ double sh[kThreads];
+  const int n = ldg(level == 1 ? &L->n1 : &L->n2);
+  if ((int)blockIdx.x >= n) return;
+  const int ti = ldg(recheck_list(L, ntensors, level) + blockIdx.x);
+  const DevTensor &t = TT[ti];
+  const int64_t ntiles = (int64_t)t.ntr * t.ntc;
+  const double S = wg_sum(t.ssum, ntiles, sh);
+  const double Q4 = level == 1 ? wg_sum(t.qsum, ntiles, sh) : 0.0;
+  if (threadIdx.x != 0) return;
+  bool amb = false;
+  const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
+  const float kf = clip_from_sum(S, (double)(t.n * t.m), k.d, spread, amb);
+  const int why = ldg(&t.sc->ambiguous) & ~0xF;
+  if (amb) {
+    const int pos = atomicAdd(&L->n2, 1);
+    stg(recheck_list(L, ntensors, 2) + pos, (int32_t)ti);
+    stg(&t.sc->ambiguous, (int32_t)(kClipPending2 | (kWhySpread << 4)));
+    return;
+  }
+  stg(&t.sc->k, kf);
+  stg(&t.sc->ambiguous, (int32_t)(why | (level == 1 ? kClipSplit : kClipExact)));
 }
 
 // --------------------------------------------------------------------------------------------
@@ -1165,25 +1247,18 @@ __global__ __launch_bounds__(kThreads) void p2_exact_kernel(const DevTensor *__r
 // is exactly 1, and above it the tensor goes to the exact pass.
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restrict__ TT,
-                                                        const Item *__restrict__ items, StepConsts k, int exact) {
+                                                        const Item *__restrict__ items, StepConsts k,
+                                                        RecheckLists *L, int ntensors) {
   __shared__ double sh[kThreads];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  if (exact && ldg(&t.sc->ambiguous) == 0) return;
   const int64_t ntiles = (int64_t)t.ntr * t.ntc;
   const double N = (double)(t.n * t.m);
-  if (exact) {
-    const double S = wg_sum(t.ssum, ntiles, sh);
-    if (threadIdx.x != 0) return;
-    const double r = sqrt(S / N) / (double)k.d;
-    const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
-    stg(&t.sc->k, (float)(1.0 / den));
-    stg(&t.sc->ambiguous, 2);
-    return;
-  }
   const float q = t.kind == kFactored ? mean_r_clamped(t, k.eps, sh) : 0.f;
   double S = 0.0, spread = 0.0;
   bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t.kind == kFactored;
+  int why = amb ? kWhyForced : 0;
+  int level = 2;   // the re-check a flagged tensor gets
   if (t.zpath) {
     const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
     const double Y = wg_sum(&t.bst->ysum, t.nzb, sh, bstride);
@@ -1219,6 +1294,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
     if (bad || !finite) {
       amb = true;
+      why = kWhyNonFinite;
       S = SU;
     } else if (have_z && lo >= k.eps) {   // nothing on the floor
       S = SU;
@@ -1228,7 +1304,11 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       spread = 1e-14;
     } else {
       S = fmin(SUf, Yf) * (1.0 + 1e-6);   // an upper bound of the oracle's sum
-      if (!(sqrt(S / N) / (double)k.d < 1.0)) amb = true;
+      if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
+        amb = true;
+        why = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
+        level = 1;   // the floor split per element decides most of these
+      }
     }
     // the next step's prediction, with a factor-2 margin on either side of the floor
     const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
@@ -1237,24 +1317,22 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     S = wg_sum(t.ssum, ntiles, sh);
     const double Q4 = wg_sum(t.qsum, ntiles, sh);
     if (threadIdx.x != 0) return;
-    spread = 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14;   // relative, on S
+    // exact second moment: the sum is already the oracle's own
+    spread = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
   }
-  const double r = sqrt(S / N) / (double)k.d;
-  const double den = (r != r) ? r : (r < 1.0 ? 1.0 : r);
-  const double kd = 1.0 / den;
-  const float kf = (float)kd;
-  if (!amb && S > 0.0 && r == r && r < 1e300 && spread > 0.0) {
-    if (fabs(r - 1.0) <= spread) amb = true;   // at the clipping threshold
-    if (r > 1.0) {
-      const double up = (double)nextafterf(kf, 3.0e38f), dn = (double)nextafterf(kf, 0.f);
-      const double mid_hi = 0.5 * ((double)kf + up), mid_lo = 0.5 * ((double)kf + dn);
-      const double tol = 0.5 * spread * kd;
-      if (fabs(kd - mid_hi) <= tol || fabs(kd - mid_lo) <= tol) amb = true;
-    }
-  }
+  const bool flagged_before = amb;
+  const float kf = clip_from_sum(S, N, k.d, spread, amb);
+  if (amb && !flagged_before) why = kWhySpread;
   stg(&t.sc->k, kf);
   stg(&t.sc->q, q);
-  stg(&t.sc->ambiguous, amb ? 1 : 0);
+  if (amb && t.kind == kFactored) {
+    int32_t *list = recheck_list(L, ntensors, level);
+    const int pos = atomicAdd(level == 1 ? &L->n1 : &L->n2, 1);
+    stg(list + pos, (int32_t)it.tensor);
+    stg(&t.sc->ambiguous, (int32_t)((level == 1 ? kClipPending1 : kClipPending2) | (why << 4)));
+  } else {
+    stg(&t.sc->ambiguous, (int32_t)kClipFast);
+  }
 }
 
 // The oracle's float sequence for one factored element (Alg. 1 with the eps clamps):
@@ -1422,7 +1500,13 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
 // p3: clip factor, state update, weight update and dithered bf16 write-back (Alg. 1)
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restrict__ TT,
-                                                      const Item *__restrict__ items, StepConsts k) {
+                                                      const Item *__restrict__ items, StepConsts k,
+                                                      RecheckLists *L) {
+  // the re-check lists of this step are consumed: empty them for the next
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    stg(&L->n1, 0);
+    stg(&L->n2, 0);
+  }
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   const Tile tl = tile_of(t, it.tile);
@@ -1475,19 +1559,30 @@ int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepCo
   hipLaunchKernelGGL(p2_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
   return (int)hipGetLastError();
 }
-int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int exact, void *stream) {
+int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
+                int ntensors, void *stream) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(clip_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, exact);
+  hipLaunchKernelGGL(clip_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, L,
+                     ntensors);
   return (int)hipGetLastError();
 }
-int launch_p2_exact(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
-  if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(p2_exact_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
+int launch_recheck(const DevTensor *T, RecheckLists *L, int ntensors, const StepConsts &k, int level, void *stream) {
+  if (ntensors <= 0) return hipSuccess;
+  hipLaunchKernelGGL(recheck_kernel, dim3(kRecheckGrid), dim3(kThreads), 0, (hipStream_t)stream, T, L, ntensors, k,
+                     level);
   return (int)hipGetLastError();
 }
-int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
+int launch_clip_recheck(const DevTensor *T, RecheckLists *L, int ntensors, const StepConsts &k, int level,
+                        void *stream) {
+  if (ntensors <= 0) return hipSuccess;
+  hipLaunchKernelGGL(clip_recheck_kernel, dim3((uint32_t)ntensors), dim3(kThreads), 0, (hipStream_t)stream, T, L,
+                     ntensors, k, level);
+  return (int)hipGetLastError();
+}
+int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
+              void *stream) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(p3_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
+  hipLaunchKernelGGL(p3_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, L);
   return (int)hipGetLastError();
 }
 

@@ -122,13 +122,37 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     items_total += tiles;
     if (items_total > INT32_MAX / 2) return SKEW_EINVAL;
   }
+  // pipeline groups: consecutive tensors, about equal algorithmic bytes (gradient, weight
+  // read and write, and the state each tier reads and writes)
+  {
+    std::vector<double> bytes(n, 0.0);
+    double total = 0.0;
+    int nonempty = 0;
+    for (int i = 0; i < n; i++) {
+      const TensorPlan &tp = p.t[i];
+      if (tp.empty) continue;
+      bytes[i] = (double)tp.N * (6.0 + (tp.momentum ? 8.0 : 0.0) + (tp.kind == kExact ? 8.0 : 0.0));
+      total += bytes[i];
+      nonempty++;
+    }
+    p.ngroups = std::max(1, std::min(kMaxGroups, nonempty));
+    p.tgroup.assign(n, 0);
+    double acc = 0.0;
+    for (int i = 0; i < n; i++) {
+      const int g = total > 0.0 ? (int)(acc / total * p.ngroups) : 0;
+      p.tgroup[i] = std::min(g, p.ngroups - 1);
+      acc += bytes[i];
+    }
+  }
   p.state_bytes = st;
-  // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][partials]
+  // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][re-check lists][partials]
   size_t ws = 0;
   p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
   p.off_items = ws;
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
                                      p.clip.size() + 1));
+  p.off_lists = ws;
+  ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(n, 1));
   auto shift = [ws](size_t &off) {
     if (off != SIZE_MAX) off += ws;
   };

@@ -22,7 +22,7 @@ ABI_VERSION = 1
 
 # names every build of the library exports (checked by the CPU test suite)
 EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
-           "skew_abi_version", "skew_timing_enable", "skew_timing_read", "skew_launch_name")
+           "skew_abi_version", "skew_timing_enable", "skew_timing_read", "skew_launch_name", "skew_clip_info")
 
 
 class SkewError(RuntimeError):
@@ -81,6 +81,9 @@ def lib():
         L.skew_timing_read.restype = ctypes.c_int
         L.skew_launch_name.argtypes = [ctypes.c_void_p, ctypes.c_int]
         L.skew_launch_name.restype = ctypes.c_char_p
+        L.skew_clip_info.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.c_int, ctypes.c_void_p]
+        L.skew_clip_info.restype = ctypes.c_int
         if L.skew_abi_version() != ABI_VERSION:
             raise RuntimeError("libskewadam.so ABI version mismatch")
         _LIB = L
@@ -189,6 +192,16 @@ class SkewAdam:
         out = {self._lib.skew_launch_name(self._ctx, j).decode(): ms[j] for j in range(nl.value)}
         out["_steps"] = ns.value
         return out
+
+    def clip_info(self, stream=None):
+        """(k, route) lists of the last step, one entry per tensor (see skew_clip_info)."""
+        n = max(1, len(self.descs))
+        k = (ctypes.c_float * n)()
+        route = (ctypes.c_int32 * n)()
+        rc = self._lib.skew_clip_info(self._ctx, k, route, n, self._stream(stream))
+        if rc != SKEW_OK:
+            raise SkewError(rc, "skew_clip_info")
+        return list(k)[:len(self.descs)], list(route)[:len(self.descs)]
 
     def state_views(self, i: int) -> dict:
         """float32 torch views of tensor i's state slices (m, v, r, c; absent ones omitted)."""

@@ -20,6 +20,7 @@ constexpr size_t kAlign = 256;
 
 // Row-band pass (pass 1 of factored matrices up to kZMaxCols columns): a work-group of
 // kZThreads threads owns whole rows, so it knows each R_i as soon as the row is summed.
+constexpr int kSub = 16;                 // update-sum passes: work-groups (row interleaves) per tile
 constexpr int kZThreads = 512;           // 8 wave64 (up to 256 VGPRs each: nothing is held in flight)
 constexpr int kZWaves = kZThreads / 64;
 constexpr int kZMaxSeg = 4;              // 512-column chunks per wave and row
@@ -27,6 +28,7 @@ constexpr int64_t kZBandElems = 1 << 21; // target elements per row band: 4 MiB 
 constexpr int kZVariants = 12;           // kernel variants: log2(nseg) * 4 + (element loads ? 2 : 0) + momentum
 constexpr int kZLdsBytes = 64 * 1024;    // one LDS staging buffer of the row-band pass (two per work-group)
 constexpr int kZMaxBlockRows = 64;       // rows staged per block, at most
+constexpr int kZMaxBandRows = 2048;      // rows per band, at most (their R are staged in LDS)
 
 // Per-tensor scalars of one step, written by the clip stage and read by the update.
 struct TensorScalars {

@@ -118,21 +118,20 @@ struct Dither {
     khi = (uint32_t)(k >> 32);
     inner0 = fmix32(khi);
   }
-  __device__ __forceinline__ uint32_t pair(uint64_t p) const {
+  // the hash input of pair p before the final mix: pair(p) = fmix32(pair_base(p))
+  __device__ __forceinline__ uint32_t pair_base(uint64_t p) const {
     const uint32_t ph = (uint32_t)(p >> 32);
     const uint32_t inner = (ph == 0u) ? inner0 : fmix32(ph ^ khi);
-    return fmix32((uint32_t)p ^ klo ^ inner);
+    return (uint32_t)p ^ klo ^ inner;
   }
+  __device__ __forceinline__ uint32_t pair(uint64_t p) const { return fmix32(pair_base(p)); }
 };
 
-// e * 2^-24 with e = 2*u16 + 1 - 2^16, for u16 = bits 7..22 of `field`:
-// the float 2^-7 (1 + (2 u16 + 1) 2^-17) minus 1.5 * 2^-7, both steps exact.
-__device__ __forceinline__ float dither_lo(uint32_t h) {
-  return __uint_as_float(0x3C000040u | ((h << 7) & 0x7FFF80u)) - 0.01171875f;
-}
-__device__ __forceinline__ float dither_hi(uint32_t h) {
-  return __uint_as_float(0x3C000040u | ((h >> 9) & 0x7FFF80u)) - 0.01171875f;
-}
+// e * 2^-24 with e = 2*u16 + 1 - 2^16 = u16 * 2^-23 + (1 - 2^16) * 2^-24: a multiple of
+// 2^-24 below 2^-8 in magnitude, so the fma is exact (u16 converts exactly)
+__device__ __forceinline__ float dither_u16(uint32_t u) { return fmaf((float)u, 0x1p-23f, -65535.0f * 0x1p-24f); }
+__device__ __forceinline__ float dither_lo(uint32_t h) { return dither_u16(h & 0xFFFFu); }
+__device__ __forceinline__ float dither_hi(uint32_t h) { return dither_u16(h >> 16); }
 __device__ __forceinline__ float dither_of(uint32_t h, uint64_t idx) { return (idx & 1u) ? dither_hi(h) : dither_lo(h); }
 
 // fixed-order tree over the work-group (every thread gets the total)
@@ -444,6 +443,7 @@ __device__ __forceinline__ void lds_write16(unsigned char *p, uint4 u) {
 
 constexpr int kZRowSlots = kZMaxBlockRows * kZWaves;   // row partials of one block: [row][wave in group]
 
+
 // Cross-lane moves of doubles without LDS: DPP within 16-lane rows (quad permutes, half
 // and full row mirrors) and the gfx950 lane-half swaps. Each reduction step adds two
 // partials that both lanes of a pair add in the same order: results are deterministic.
@@ -515,7 +515,8 @@ __device__ __forceinline__ double rsq_d(double x) {
 
 template <int NSEG, int RB, bool MOM, bool VEC>
 __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, unsigned char *bufA,
-                                         unsigned char *bufB, float *rbA, float *rbB, double *rowsh, double *sh) {
+                                         unsigned char *bufB, float *rbA, float *rbB, double *rowsh, double *sh,
+                                         float *rstash) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
@@ -557,9 +558,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
     for (int e = 0; e < 8; e++) cacc[s][e] = zacc[s][e] = 0.0;
   double ysum = 0.0, umax = 0.0;
-  // R statistics, kept by lane b * P of the group's first wave for its rows
-  double rs_l = 0.0;
-  float rmn_l = __builtin_inff(), rmx_l = 0.f;
+  // a row with R_i == 0 but a nonzero sum (flagged by lane b * P of the group's first wave)
   int bad_l = 0;
 
   // Block loads: piece p = (row r, chunk c) of the block goes to wave p % 8. Rows past
@@ -689,11 +688,9 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       const bool normal = R > 0.f && R < __builtin_inff();
       winv_l = R > 0.f ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
       if (active && wg == 0 && b < rb && w == 0 && i < r1) {
-        stg(t.R + i, R);
-        stg(t.ainv + i, normal ? rsq_d(Rd) : 1.0 / sqrt(Rd));
-        rs_l += Rd;
-        if (R > 0.f) rmn_l = fminf(rmn_l, R);
-        rmx_l = fmaxf(rmx_l, R);
+        // staged for the band's end: a global store here would hold up the next block's
+        // wait for its staged rows until the store completes
+        rstash[i - r0] = R;
         if (R != R || (!(R > 0.f) && x > 0.0)) bad_l = 1;
       }
     }
@@ -807,47 +804,33 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       }
     }
   }
-  // band statistics: the R statistics sit in lanes b * P of each group's first wave, in
-  // row order; combined in (group, row) order
+  // the band's R and 1/sqrt(R) (coalesced), and its statistics: fixed-order reductions
+  const int64_t nrows = r1 - r0;
+  double rs = 0.0;
+  float rmn = __builtin_inff(), rmx = 0.f;
+  for (int64_t j = threadIdx.x; j < nrows; j += kZThreads) {
+    const float R = rstash[j];
+    const double Rd = (double)R;
+    const bool normal = R > 0.f && R < __builtin_inff();
+    stg(t.R + r0 + j, R);
+    stg(t.ainv + r0 + j, normal ? rsq_d(Rd) : 1.0 / sqrt(Rd));
+    rs += Rd;
+    if (R > 0.f) rmn = fminf(rmn, R);
+    rmx = fmaxf(rmx, R);
+  }
   const double ys = wg_sum_w<kZWaves>(ysum, sh);
   const double um = wg_max_w<kZWaves>(umax, sh);
-  double *gs = sh + kZWaves;
-  if (active && wg == 0) {
-    double rs = 0.0;
-    float rmn = __builtin_inff(), rmx = 0.f;
-    int bd = 0;
-    for (int b = 0; b < rb; b++) {
-      const int src = b * P;
-      rs += __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(rs_l), src),
-                             __builtin_amdgcn_readlane(__double2loint(rs_l), src));
-      rmn = fminf(rmn, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rmn_l), src)));
-      rmx = fmaxf(rmx, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rmx_l), src)));
-      bd |= __builtin_amdgcn_readlane(bad_l, src);
-    }
-    if (lane == 0) {
-      gs[grp] = rs;
-      gs[kZWaves + grp] = (double)rmn;
-      gs[2 * kZWaves + grp] = (double)rmx;
-      gs[3 * kZWaves + grp] = (double)bd;
-    }
-  }
-  __syncthreads();
+  const double rsum = wg_sum_w<kZWaves>(rs, sh);
+  const float rmin = wg_min_wf<kZWaves>(rmn, sh);
+  const float rmax = wg_max_wf<kZWaves>(rmx, sh);
+  const int bd = wg_or_w<kZWaves>(bad_l, sh);
   if (threadIdx.x == 0) {
-    double rsum = 0.0;
-    float rmin = __builtin_inff(), rmax = 0.f;
-    int b = 0;
-    for (int g = 0; g < rpi; g++) {
-      rsum += gs[g];
-      rmin = fminf(rmin, (float)gs[kZWaves + g]);
-      rmax = fmaxf(rmax, (float)gs[2 * kZWaves + g]);
-      b |= gs[3 * kZWaves + g] != 0.0 ? 1 : 0;
-    }
     stg(&t.bst[band].rsum, rsum);
     stg(&t.bst[band].ysum, ys);
     stg(&t.bst[band].umax, um);
     stg(&t.bst[band].rmin, rmin);
     stg(&t.bst[band].rmax, rmax);
-    stg(&t.bst[band].bad, b);
+    stg(&t.bst[band].bad, bd);
     stg(&t.bst[band].regime, (int32_t)regime);
   }
 }
@@ -860,16 +843,17 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   __shared__ float rbA[64], rbB[64];
   __shared__ double rowsh[2 * kZRowSlots];
   __shared__ double sh[5 * kZWaves];
+  __shared__ float rstash[kZMaxBandRows];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   // rows per group and block: the planner keeps 4 at most with one chunk per wave, 2 with
   // two and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG == 1 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else
-    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh);
+    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
 }
 
 // fixed-order work-group sum of p[0], p[stride], ..., p[(n-1) stride]: thread j sums
@@ -983,8 +967,10 @@ struct SumPair {
   double s, q4;
 };
 
-__device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float q) {
+__device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &tl, int part, const StepConsts &k,
+                                               float q) {
   const WaveMap wm(t, tl);
+  const int64_t r0 = wm.wr + (int64_t)part * wm.rpi, rs = (int64_t)wm.rpi * kSub;   // this part's rows
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
   const float s = mom ? k.s_m : k.s_0;
@@ -1011,9 +997,9 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
     a.q4 = fma(u2, u2, a.q4);
   };
   if (t.vec) {
-    for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
-      const bool two = lr + wm.rpi < tl.nr;
-      const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + wm.rpi) : i;
+    for (int64_t lr = r0; lr < tl.nr; lr += 2 * rs) {
+      const bool two = lr + rs < tl.nr;
+      const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + rs) : i;
       const uint4 ga = ldg(reinterpret_cast<const uint4 *>(t.g + i * ld + col));
       const uint4 gb = ldg(reinterpret_cast<const uint4 *>(t.g + i2 * ld + col));
       float ma[8], mb[8];
@@ -1047,7 +1033,7 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
       }
     }
   } else {
-    for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+    for (int64_t lr = r0; lr < tl.nr; lr += rs) {
       const int64_t i = tl.row(lr);
       const float Ri = ldg(t.R + i);
       const double ai = ldg(t.ainv + i);
@@ -1065,9 +1051,10 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
 
 // The oracle's own float sequence for U_hat of a factored tensor, summed in double:
 // used when the approximate sum leaves the clip factor's rounding undecided.
-__device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Tile &tl, const StepConsts &k,
-                                                    float q) {
+__device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Tile &tl, int part,
+                                                    const StepConsts &k, float q) {
   const WaveMap wm(t, tl);
+  const int64_t r0 = wm.wr + (int64_t)part * wm.rpi, rs = (int64_t)wm.rpi * kSub;
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
   const float s = mom ? k.s_m : k.s_0;
@@ -1076,7 +1063,7 @@ __device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Ti
   float cp[8];
 #pragma unroll
   for (int e = 0; e < 8; e++) cp[e] = (col + e < m) ? ldg(t.C + col + e) / q : 0.f;
-  for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+  for (int64_t lr = r0; lr < tl.nr; lr += rs) {
     const int64_t i = tl.row(lr);
     const float Ri = ldg(t.R + i);
 #pragma unroll
@@ -1091,13 +1078,14 @@ __device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Ti
   return acc;
 }
 
-__device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, const StepConsts &k) {
+__device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, int part, const StepConsts &k) {
   // exact second moment (router tier, vectors): the oracle's operation order exactly
   const WaveMap wm(t, tl);
+  const int64_t r0 = wm.wr + (int64_t)part * wm.rpi, rs = (int64_t)wm.rpi * kSub;
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
   double acc = 0.0;
-  for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
+  for (int64_t lr = r0; lr < tl.nr; lr += rs) {
     const int64_t i = tl.row(lr);
 #pragma unroll
     for (int e = 0; e < 8; e++) {
@@ -1117,15 +1105,16 @@ __device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, c
 __global__ __launch_bounds__(kThreads) void p2_kernel(const DevTensor *__restrict__ TT,
                                                       const Item *__restrict__ items, StepConsts k) {
   __shared__ double sh[kThreads];
-  const Item it = items[blockIdx.x];
+  const Item it = items[blockIdx.x];   // it.tile = tile * kSub + part
   const DevTensor &t = TT[it.tensor];
-  const Tile tl = tile_of(t, it.tile);
+  const Tile tl = tile_of(t, it.tile / kSub);
+  const int part = it.tile % kSub;
   SumPair acc;
   if (t.kind == kFactored) {
     const float q = mean_r_clamped(t, k.eps, sh);
-    acc = p2_factored(t, tl, k, q);
+    acc = p2_factored(t, tl, part, k, q);
   } else {
-    acc.s = p2_exact(t, tl, k);   // already the oracle's own U_hat
+    acc.s = p2_exact(t, tl, part, k);   // already the oracle's own U_hat
     acc.q4 = 0.0;
   }
   const double s = block_sum(acc.s, sh);
@@ -1154,23 +1143,24 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
   int64_t total = 0;
   for (int j = 0; j < n; j++) {
     const DevTensor &t = TT[ldg(list + j)];
-    total += (int64_t)t.ntr * t.ntc;
+    total += (int64_t)t.ntr * t.ntc * kSub;
   }
   for (int64_t idx = blockIdx.x; idx < total; idx += gridDim.x) {
     int64_t base = 0;
     int j = 0;
     for (;; j++) {
       const DevTensor &t = TT[ldg(list + j)];
-      const int64_t nt = (int64_t)t.ntr * t.ntc;
+      const int64_t nt = (int64_t)t.ntr * t.ntc * kSub;
       if (idx < base + nt) break;
       base += nt;
     }
     const DevTensor &t = TT[ldg(list + j)];
-    const int tile = (int)(idx - base);
-    const Tile tl = tile_of(t, tile);
+    const int tile = (int)(idx - base);   // tile * kSub + part
+    const Tile tl = tile_of(t, tile / kSub);
+    const int part = tile % kSub;
     const float q = mean_r_clamped(t, k.eps, sh);
     if (level == 1) {
-      const SumPair acc = p2_factored(t, tl, k, q);
+      const SumPair acc = p2_factored(t, tl, part, k, q);
       const double sv = block_sum(acc.s, sh);
       const double q4 = block_sum(acc.q4, sh);
       if (threadIdx.x == 0) {
@@ -1178,7 +1168,7 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
         stg(t.qsum + tile, q4);
       }
     } else {
-      const double sv = block_sum(p2_factored_exact(t, tl, k, q), sh);
+      const double sv = block_sum(p2_factored_exact(t, tl, part, k, q), sh);
       if (threadIdx.x == 0) stg(t.ssum + tile, sv);
     }
   }
@@ -1213,7 +1203,7 @@ __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor 
   if ((int)blockIdx.x >= n) return;
   const int ti = ldg(recheck_list(L, ntensors, level) + blockIdx.x);
   const DevTensor &t = TT[ti];
-  const int64_t ntiles = (int64_t)t.ntr * t.ntc;
+  const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
   const double S = wg_sum(t.ssum, ntiles, sh);
   const double Q4 = level == 1 ? wg_sum(t.qsum, ntiles, sh) : 0.0;
   if (threadIdx.x != 0) return;
@@ -1252,7 +1242,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   __shared__ double sh[kThreads];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  const int64_t ntiles = (int64_t)t.ntr * t.ntc;
+  const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
   const double N = (double)(t.n * t.m);
   const float q = t.kind == kFactored ? mean_r_clamped(t, k.eps, sh) : 0.f;
   double S = 0.0, spread = 0.0;
@@ -1345,13 +1335,16 @@ __device__ __forceinline__ float exact_factored_y(float x, float w, float Ri, fl
   return fmaf(dith, fabsf(w), fmaf(-lr, U, w));
 }
 
-// True when y may round differently from the oracle's value: the fast update x*F differs
-// from the oracle's lr*U by < 2^-19 relative, and each of x and y carries one rounding.
-__device__ __forceinline__ bool near_boundary(float y, float xF, float w) {
-  const float mid = __uint_as_float((__float_as_uint(y) & 0xFFFF0000u) | 0x8000u);
+// y may round differently from the oracle's value when this is >= 0: the fast update x*F
+// differs from the oracle's lr*U by < 2^-19 relative, and each of x and y carries one
+// rounding. (y - mid is exact and finite for finite y; NaN never counts as near.)
+__device__ __forceinline__ float boundary_slack(float y, float xF, float w) {
+  // the midpoint between y's two bf16 neighbours: y's high half, then 0x8000
+  const float mid = __uint_as_float(__builtin_amdgcn_perm(__float_as_uint(y), 0x8000u, 0x07060100u));
   const float bound = fmaf(fabsf(xF), 0x1p-18f + 0x1p-21f, fabsf(w) * 0x1p-21f);
-  return fabsf(y - mid) <= bound;
+  return bound - fabsf(y - mid);
 }
+__device__ __forceinline__ bool near_boundary(float y, float xF, float w) { return boundary_slack(y, xF, w) >= 0.f; }
 
 struct P3Scalars {
   float q, s, kc, cap3, eps, lr;
@@ -1374,22 +1367,26 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
     store_m8(t.M + i * t.m + col, x);
   }
   const float alpha = (float)(c.lsk * ldg(t.ainv + i));
-  const uint64_t p0 = ((uint64_t)i * (uint64_t)t.m + (uint64_t)col) >> 1;   // m and col are even here
+  // pairs p0 .. p0 + 3: m and col are multiples of 8, so p0 is a multiple of 4 and the
+  // four pairs share their high word and differ only in the low two bits
+  const uint64_t p0 = ((uint64_t)i * (uint64_t)t.m + (uint64_t)col) >> 1;
+  // pair indices reach 2^32 only in tensors of more than 2^33 elements (a uniform test)
+  const uint32_t base = (t.n * t.m > (int64_t(1) << 33)) ? dz.pair_base(p0) : ((uint32_t)p0 ^ dz.klo ^ dz.inner0);
   float y[8], dith[8];
-  bool any = false;
 #pragma unroll
   for (int e2 = 0; e2 < 4; e2++) {
-    const uint32_t h = dz.pair(p0 + e2);
+    const uint32_t h = fmix32(base ^ (uint32_t)e2);
     dith[2 * e2] = dither_lo(h);
     dith[2 * e2 + 1] = dither_hi(h);
   }
+  float slack = -1.f;
 #pragma unroll
   for (int e = 0; e < 8; e++) {
     const float F = fminf(alpha * bf[e], c.cap3);
     y[e] = fmaf(dith[e], fabsf(w[e]), fmaf(-x[e], F, w[e]));
-    any |= near_boundary(y[e], x[e] * F, w[e]);
+    slack = fmaxf(slack, boundary_slack(y[e], x[e] * F, w[e]));
   }
-  if (any) {
+  if (slack >= 0.f) {
     const float Ri = ldg(t.R + i);
 #pragma unroll
     for (int e = 0; e < 8; e++) {

@@ -60,13 +60,13 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     const int64_t tc = (int64_t)kChunk * tp.cw;
     tp.tr = std::max<int64_t>(1, kTileElems / tc);
     const int64_t ntc = ceil_div(tp.m, tc), ntr = ceil_div(tp.n, tp.tr);
-    if (ntc * ntr > INT32_MAX / 2) return SKEW_EINVAL;
+    if (ntc * ntr > INT32_MAX / 2 / kSub) return SKEW_EINVAL;   // tile * kSub + part fits an int32
     tp.ntc = (int32_t)ntc;
     tp.ntr = (int32_t)ntr;
     const int64_t tiles = ntc * ntr;
 
-    tp.off_ssum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
-    tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * 8);
+    tp.off_ssum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
+    tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
     tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
     p.clip.push_back({i, 0});
     // Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
@@ -88,6 +88,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.zrb = (int32_t)zrb;
       const int64_t rows_block = rpi * zrb;
       tp.zrows = ceil_div(std::max<int64_t>(1, ceil_div(kZBandElems, tp.m)), rows_block) * rows_block;
+      tp.zrows = std::min<int64_t>(tp.zrows, kZMaxBandRows / rows_block * rows_block);
       const int64_t nzb = ceil_div(tp.n, tp.zrows), nfc = ceil_div(tp.m, kFold);
       if (nzb > INT32_MAX / 2 || nfc > INT32_MAX / 2) return SKEW_EINVAL;
       tp.nzb = (int32_t)nzb;
@@ -115,8 +116,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       items_total += tiles + nfr + nfc;
     }
     if (!tp.zpath) {
-      for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p2.push_back({i, k});
-      items_total += tiles;
+      for (int32_t k = 0; k < tp.ntr * tp.ntc * kSub; k++) p.p2.push_back({i, k});   // tile * kSub + part
+      items_total += tiles * kSub;
     }
     for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p3.push_back({i, k});
     items_total += tiles;

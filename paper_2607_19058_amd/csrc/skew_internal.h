@@ -15,12 +15,12 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 512;             // columns one wave covers with one 16-byte load per lane
 constexpr int kMaxCw = 4;               // chunks per tile row: 1, 2 or 4 (at most 2048 columns)
 constexpr int kFold = 256;              // rows (or columns) folded by one work-group
-constexpr int64_t kTileElems = 1 << 19; // target elements per tile: 1 MiB of bf16 gradient
+constexpr int64_t kTileElems = 1 << 16; // target elements per tile: 128 KiB of bf16 gradient
 constexpr size_t kAlign = 256;
 
 // Row-band pass (pass 1 of factored matrices up to kZMaxCols columns): a work-group of
 // kZThreads threads owns whole rows, so it knows each R_i as soon as the row is summed.
-constexpr int kSub = 16;                 // update-sum passes: work-groups (row interleaves) per tile
+constexpr int kSub = 2;                  // update-sum passes: work-groups (row interleaves) per tile
 constexpr int kZThreads = 512;           // 8 wave64 (up to 256 VGPRs each: nothing is held in flight)
 constexpr int kZWaves = kZThreads / 64;
 constexpr int kZMaxSeg = 4;              // 512-column chunks per wave and row

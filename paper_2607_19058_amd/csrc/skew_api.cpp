@@ -149,6 +149,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.ssum = reinterpret_cast<double *>(ws + tp.off_ssum);
     x.qsum = reinterpret_cast<double *>(ws + tp.off_qsum);
     x.sc = reinterpret_cast<TensorScalars *>(ws + tp.off_sc);
+    x.zeros = reinterpret_cast<const uint16_t *>(ws + p.off_zero);
     auto wsp = [&](size_t off) { return off == SIZE_MAX ? nullptr : static_cast<void *>(ws + off); };
     x.rowpart = static_cast<double *>(wsp(tp.off_rowpart));
     x.colpart = static_cast<double *>(wsp(tp.off_colpart));

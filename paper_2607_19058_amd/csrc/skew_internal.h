@@ -104,6 +104,7 @@ struct DevTensor {
   double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
   double *qsum;           // [ntr*ntc]  per-tile sums of U_hat^4 over the approximated elements
   TensorScalars *sc;      // this step's clip factor and reconstruction clamp
+  const uint16_t *zeros;  // 256 zero bytes (never written): the source of padding loads
   int64_t n, m, ld;       // rows, columns, row stride (elements)
   int64_t tr;             // rows per tile
   int32_t cw;             // 512-column chunks per tile (1, 2 or 4)
@@ -165,6 +166,7 @@ constexpr int kMaxGroups = 1;
 struct Plan {
   std::vector<TensorPlan> t;
   size_t off_lists = 0;                       // workspace offset of the RecheckLists
+  size_t off_zero = 0;                        // workspace offset of 256 zero bytes
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
   std::vector<Item> z;                        // row-band pass items (split by kernel variant at init)
   int32_t ngroups = 1;

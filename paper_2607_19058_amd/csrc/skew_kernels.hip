@@ -453,8 +453,9 @@ constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i within each 8 lanes
 constexpr int kDppMirror = 0x140;     // lane i <-> 15 - i within each 16 lanes
 template <int CTRL>
 __device__ __forceinline__ double dpp_d(double x) {
-  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xF, 0xF, false);
+  // every lane reads a defined source lane under these patterns: no old value is needed
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(x), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(x), CTRL, 0xF, 0xF, false);
   return __hiloint2double(hi, lo);
 }
 // a, b -> lanes < 32: a[l] + a[l + 32]; lanes >= 32: b[l - 32] + b[l]
@@ -516,7 +517,7 @@ __device__ __forceinline__ double rsq_d(double x) {
 template <int NSEG, int RB, bool MOM, bool VEC>
 __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, unsigned char *bufA,
                                          unsigned char *bufB, float *rbA, float *rbB, double *rowsh, double *sh,
-                                         float *rstash) {
+                                         float *rstash, const unsigned char *zlds) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
@@ -557,38 +558,41 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   for (int s = 0; s < NSEG; s++)
 #pragma unroll
     for (int e = 0; e < 8; e++) cacc[s][e] = zacc[s][e] = 0.0;
-  double ysum = 0.0, umax = 0.0;
+  double ysum = 0.0, ysum2 = 0.0, umax = 0.0;   // the floored sum in two chains
   // a row with R_i == 0 but a nonzero sum (flagged by lane b * P of the group's first wave)
   int bad_l = 0;
 
   // Block loads: piece p = (row r, chunk c) of the block goes to wave p % 8. Rows past
-  // the band's end and lanes past the row's end load a valid address; their slots are
-  // never used. Wave 0 also stages the block's old R values.
+  // the band's end and lanes past the row's end load zeros (from a zero block in global
+  // memory), so they add nothing to any sum and the sweeps need no masks. Wave 0 also
+  // stages the block's old R values.
   const int pr0 = wave / zcw, pc0 = wave - pr0 * zcw;                   // piece `wave`: (row, chunk)
   const int dr = kZWaves / zcw, dc = kZWaves - (kZWaves / zcw) * zcw;   // step of 8 pieces
   auto issue = [&](int64_t blk, unsigned char *buf, float *rbuf) {
     const int64_t rbase = r0 + blk * br;
     int r = pr0, c = pc0;
     for (int p = wave; p < npieces; p += kZWaves) {
-      const int64_t i = (rbase + r < r1) ? rbase + r : r1 - 1;
+      const bool rok = rbase + r < r1;   // wave-uniform
+      const int64_t i = rok ? rbase + r : r1 - 1;
       const int64_t cg = (int64_t)c * kChunk + lane * 8;
       if (VEC) {
-        dma16(t.g + i * ld + (cg < m ? cg : 0), buf + (size_t)p * 1024);
+        dma16((rok && cg < m) ? (const void *)(t.g + i * ld + cg) : (const void *)t.zeros, buf + (size_t)p * 1024);
       } else {
-        lds_write16(buf + (size_t)p * 1024 + lane * 16, load_bf8(t.g, ld, m, i, cg));
+        lds_write16(buf + (size_t)p * 1024 + lane * 16, rok ? load_bf8(t.g, ld, m, i, cg) : make_uint4(0u, 0u, 0u, 0u));
       }
       if (MOM) {
         const float *mrow = t.M + i * m;
         const int64_t c0 = (int64_t)c * kChunk + lane * 4, c1 = c0 + 256;
         if (VEC) {
-          dma16(mrow + (c0 < m ? c0 : 0), buf + goff_m + (size_t)p * 2048);
-          dma16(mrow + (c1 < m ? c1 : 0), buf + goff_m + (size_t)p * 2048 + 1024);
+          dma16((rok && c0 < m) ? (const void *)(mrow + c0) : (const void *)t.zeros, buf + goff_m + (size_t)p * 2048);
+          dma16((rok && c1 < m) ? (const void *)(mrow + c1) : (const void *)t.zeros,
+                buf + goff_m + (size_t)p * 2048 + 1024);
         } else {
           uint32_t mv[8];
 #pragma unroll
           for (int e = 0; e < 4; e++) {
-            mv[e] = (c0 + e < m) ? __float_as_uint(ldg(mrow + c0 + e)) : 0u;
-            mv[4 + e] = (c1 + e < m) ? __float_as_uint(ldg(mrow + c1 + e)) : 0u;
+            mv[e] = (rok && c0 + e < m) ? __float_as_uint(ldg(mrow + c0 + e)) : 0u;
+            mv[4 + e] = (rok && c1 + e < m) ? __float_as_uint(ldg(mrow + c1 + e)) : 0u;
           }
           lds_write16(buf + goff_m + (size_t)p * 2048 + lane * 16, make_uint4(mv[0], mv[1], mv[2], mv[3]));
           lds_write16(buf + goff_m + (size_t)p * 2048 + 1024 + lane * 16, make_uint4(mv[4], mv[5], mv[6], mv[7]));
@@ -611,26 +615,18 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     }
   };
   // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (four
-  // 16-byte reads in flight together); zero where the lane has no column or the row is
-  // past the band's end.
+  // 16-byte reads in flight together). Staged padding is zero; a segment past the row's
+  // last chunk (wave-uniform) reads the zero area instead.
   constexpr int RBB = (4 / NSEG < RB ? 4 / NSEG : RB) > 0 ? (4 / NSEG < RB ? 4 / NSEG : RB) : 1;
-  auto read_rows = [&](const unsigned char *buf, int64_t rbase, int b0, uint4 (&u)[RBB][NSEG]) {
+  auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&u)[RBB][NSEG]) {
     const unsigned char *ptr[RBB * NSEG];
-    uint4 v[RBB * NSEG];
 #pragma unroll
     for (int b = 0; b < RBB; b++)
 #pragma unroll
-      for (int s = 0; s < NSEG; s++) {
-        const int ch = chs[s] < zcw ? chs[s] : 0;
-        ptr[b * NSEG + s] = buf + (size_t)((grp_c * RB + b0 + b) * zcw + ch) * 1024 + lane * 16;
-      }
-    lds_read16_n<RBB * NSEG>(ptr, v);
-#pragma unroll
-    for (int b = 0; b < RBB; b++) {
-      const bool rv = active && rbase + grp_c * RB + b0 + b < r1;
-#pragma unroll
-      for (int s = 0; s < NSEG; s++) u[b][s] = (rv && sok[s]) ? v[b * NSEG + s] : make_uint4(0u, 0u, 0u, 0u);
-    }
+      for (int s = 0; s < NSEG; s++)
+        ptr[b * NSEG + s] = (chs[s] < zcw ? buf + (size_t)((grp_c * RB + b0 + b) * zcw + chs[s]) * 1024 : zlds) +
+                            lane * 16;
+    lds_read16_n<RBB * NSEG>(ptr, reinterpret_cast<uint4(&)[RBB * NSEG]>(u));
   };
   auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt) {
     __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
@@ -638,17 +634,18 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
     const int64_t rbase = r0 + blk * br;
     double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
-    // row and column sums of g^2 (bf16 squares are exact in double)
+    // row and column sums of g^2 (bf16 squares are exact in double); an idle wave's
+    // accumulators are never used
     {
       double rp[RB];
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
         uint4 u[RBB][NSEG];
-        read_rows(cur, rbase, b0, u);
+        read_rows(cur, b0, u);
 #pragma unroll
         for (int bb = 0; bb < RBB; bb++) {
           const int b = b0 + bb;
-          rp[b] = 0.0;
+          double ra = 0.0, rb2 = 0.0;   // two chains per row
 #pragma unroll
           for (int s = 0; s < NSEG; s++) {
             // one 8-element group at a time (the scheduler would otherwise convert every
@@ -659,10 +656,18 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
             for (int e = 0; e < 8; e++) {
               const double xd = (double)x[e];
-              rp[b] = fma(xd, xd, rp[b]);
+              if (e & 1)
+                rb2 = fma(xd, xd, rb2);
+              else
+                ra = fma(xd, xd, ra);
               cacc[s][e] = fma(xd, xd, cacc[s][e]);
             }
+            // the column sums are formed here, not sunk towards the loop's end (which
+            // would keep every converted element live across the block)
+#pragma unroll
+            for (int e = 0; e < 8; e++) asm volatile("" : "+v"(cacc[s][e]));
           }
+          rp[b] = ra + rb2;
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -686,7 +691,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, rcur[r]));
       const double Rd = (double)R;
       const bool normal = R > 0.f && R < __builtin_inff();
-      winv_l = R > 0.f ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
+      winv_l = (R > 0.f && i < r1) ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
       if (active && wg == 0 && b < rb && w == 0 && i < r1) {
         // staged for the band's end: a global store here would hold up the next block's
         // wait for its staged rows until the store completes
@@ -700,13 +705,12 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
       uint4 ub[RBB][NSEG];
-      read_rows(cur, rbase, b0, ub);
+      read_rows(cur, b0, ub);
 #pragma unroll
       for (int bb = 0; bb < RBB; bb++) {
         const int b = b0 + bb;
         const uint4 (&u)[RBB][NSEG] = ub;
         const int r = grp_c * rb + b;
-        const bool rv = active && rbase + r < r1;
         const int src = b * P;
         const double winv = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(winv_l), src),
                                              __builtin_amdgcn_readlane(__double2loint(winv_l), src));
@@ -717,17 +721,16 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
           float x[8];
           unpack8(u[bb][s], x);
           if (MOM) {
-            const int ch = chs[s] < zcw ? chs[s] : 0;
-            const unsigned char *mp = cur + goff_m + (size_t)(r * zcw + ch) * 2048 + lane * 32;
+            const unsigned char *mp =
+                (chs[s] < zcw ? cur + goff_m + (size_t)(r * zcw + chs[s]) * 2048 : zlds) + lane * 32;
             const unsigned char *mpp[2] = {mp, mp + 16};
             uint4 mv[2];
             lds_read16_n<2>(mpp, mv);
-            const bool ok = rv && sok[s];
             const float mo[8] = {__uint_as_float(mv[0].x), __uint_as_float(mv[0].y), __uint_as_float(mv[0].z),
                                  __uint_as_float(mv[0].w), __uint_as_float(mv[1].x), __uint_as_float(mv[1].y),
                                  __uint_as_float(mv[1].z), __uint_as_float(mv[1].w)};
 #pragma unroll
-            for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, ok ? mo[e] : 0.f));
+            for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mo[e]));
           }
 #pragma unroll
           for (int e = 0; e < 8; e++) {
@@ -740,7 +743,10 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
             if (Y) {
               const float q0 = ax * reps;
               const float uf = fmaf(fmaf(-q0, deps, ax), reps, q0);   // RN(ax / deps)
-              ysum = fma((double)uf, (double)uf, ysum);
+              if (e & 1)
+                ysum2 = fma((double)uf, (double)uf, ysum2);
+              else
+                ysum = fma((double)uf, (double)uf, ysum);
             }
           }
         }
@@ -749,7 +755,9 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       }
       __builtin_amdgcn_sched_barrier(0);
     };
-    if (want_z && want_y)
+    if (!active)
+      ;   // an idle wave (its rows are group 0's) adds nothing
+    else if (want_z && want_y)
       sweep2(std::true_type(), std::true_type());
     else if (want_z)
       sweep2(std::true_type(), std::false_type());
@@ -818,7 +826,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     if (R > 0.f) rmn = fminf(rmn, R);
     rmx = fmaxf(rmx, R);
   }
-  const double ys = wg_sum_w<kZWaves>(ysum, sh);
+  const double ys = wg_sum_w<kZWaves>(ysum + ysum2, sh);
   const double um = wg_max_w<kZWaves>(umax, sh);
   const double rsum = wg_sum_w<kZWaves>(rs, sh);
   const float rmin = wg_min_wf<kZWaves>(rmn, sh);
@@ -844,16 +852,19 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   __shared__ double rowsh[2 * kZRowSlots];
   __shared__ double sh[5 * kZWaves];
   __shared__ float rstash[kZMaxBandRows];
+  __shared__ __attribute__((aligned(16))) unsigned char zlds[2048];   // zeros: 32 bytes per lane
+  reinterpret_cast<uint32_t *>(zlds)[threadIdx.x] = 0u;   // complete before the first block's wait
+  static_assert(kZThreads * 4 == 2048, "one word per thread");
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   // rows per group and block: the planner keeps 4 at most with one chunk per wave, 2 with
   // two and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG == 1 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else
-    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
 }
 
 // fixed-order work-group sum of p[0], p[stride], ..., p[(n-1) stride]: thread j sums

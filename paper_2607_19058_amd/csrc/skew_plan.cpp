@@ -154,6 +154,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
                                      p.clip.size() + 1));
   p.off_lists = ws;
   ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(n, 1));
+  p.off_zero = ws;   // zero-filled with the workspace at set-up and never written
+  ws = align_up(ws + 256);
   auto shift = [ws](size_t &off) {
     if (off != SIZE_MAX) off += ws;
   };

@@ -857,10 +857,10 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   static_assert(kZThreads * 4 == 2048, "one word per thread");
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  // rows per group and block: the planner keeps 4 at most with one chunk per wave, 2 with
-  // two and 1 with four, which keeps every variant's loop free of register spills
-  if (NSEG == 1 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG == 1 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+  // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
+  // and 1 with four, which keeps every variant's loop free of register spills
+  if (NSEG <= 2 && t.zrb >= 4)
+    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else if (NSEG <= 2 && t.zrb >= 2)
     p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else

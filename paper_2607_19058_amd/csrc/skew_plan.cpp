@@ -78,7 +78,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     const int64_t wpr = ceil_div(zcw, nseg);
     const int64_t row_kb = zcw * (tp.momentum ? 3 : 1);   // staged KiB per row
     const int64_t rpi = wpr <= kZWaves ? kZWaves / wpr : 0;
-    int64_t zrb = rpi > 0 ? std::min<int64_t>(4 / nseg, kZLdsBytes / (rpi * row_kb * 1024)) : 0;
+    int64_t zrb = rpi > 0 ? std::min<int64_t>(nseg <= 2 ? 4 : 1, kZLdsBytes / (rpi * row_kb * 1024)) : 0;
     while (zrb & (zrb - 1)) zrb &= zrb - 1;   // a power of two: 1, 2 or 4
     tp.zpath = (tp.kind == kFactored && rpi > 0 && zrb >= 1) ? 1 : 0;
     if (tp.zpath) {

@@ -14,9 +14,9 @@ using namespace skew;
 
 namespace {
 constexpr int kLaunches = 9;
-const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_stats_other", "p1_rowcol_sumsq",
+const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_stats_momentum", "p1_rowcol_sumsq",
                                              "fold_rc_ema", "p2_update_sumsq", "clip_factor",
-                                             "p2_exact_recheck", "clip_factor_recheck", "p3_apply_dither"};
+                                             "recheck_update_sumsq", "clip_factor_recheck", "p3_apply_dither"};
 }  // namespace
 
 // an item list with the bounds of each pipeline group in it
@@ -270,7 +270,7 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
     // pass 1, fold and clip stage of group g on the caller's stream
     for (int v = 0; v < kZVariants; v++)
       if (ctx->z[v].count(g) > 0)
-        run(v == 0 ? 0 : 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, s0); });
+        run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, s0); });
     if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
     if (ctx->fold.count(g) > 0) run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, s0); });
     if (ctx->p2.count(g) > 0) run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });

@@ -56,6 +56,7 @@ class _HParams(ctypes.Structure):
         ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
         ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float),
         ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
+        ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float), ("gsq_total", ctypes.c_double),
     ]
 
 
@@ -70,6 +71,9 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         L.skew_oracle_step.argtypes = [ctypes.POINTER(_HParams), ctypes.POINTER(_Tensor), ctypes.c_int]
         L.skew_oracle_step.restype = ctypes.c_int
+        L.skew_oracle_step_gcoef.argtypes = [ctypes.POINTER(_HParams), ctypes.POINTER(_Tensor), ctypes.c_int,
+                                             ctypes.POINTER(ctypes.c_float)]
+        L.skew_oracle_step_gcoef.restype = ctypes.c_int
         L.skew_oracle_f32_to_bf16.argtypes = [ctypes.c_float]
         L.skew_oracle_f32_to_bf16.restype = ctypes.c_uint16
         L.skew_oracle_f32_to_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
@@ -135,8 +139,14 @@ class Tensor:
 def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAULTS["lr"],
          beta1: float = DEFAULTS["beta1"], beta2: float = DEFAULTS["beta2"], eps: float = DEFAULTS["eps"],
          clip_threshold: float = DEFAULTS["clip_threshold"], want_u: bool = False, want_x: bool = False,
-         want_y: bool = False) -> int:
-    """Run one oracle step over ``tensors`` in place. Returns the C status."""
+         want_y: bool = False, weight_decay: float = 0.0, max_grad_norm: float = 0.0,
+         gsq_total: Optional[float] = None) -> int:
+    """Run one oracle step over ``tensors`` in place. Returns the C status.
+
+    weight_decay: lambda of the decoupled decay (router tier exempt). max_grad_norm > 0
+    scales every gradient by min(1, max_grad_norm / (||G|| + 1e-6)) over all the tensors
+    given, or over a larger set whose sum of squares is ``gsq_total``. The scale used is
+    returned by ``last_gcoef()``."""
     tensors = list(tensors)
     arr = (_Tensor * max(1, len(tensors)))()
     rms = np.full(max(1, len(tensors)), np.nan, np.float64)
@@ -166,11 +176,23 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
                          _ptr(t.r), _ptr(t.c), _ptr(t.u_out), _ptr(t.x_out), _ptr(t.y_out),
                          rms.ctypes.data + 8 * k)
         keep.append(t)
-    hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1))
-    rc = lib().skew_oracle_step(ctypes.byref(hp), arr, len(tensors))
+    hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1),
+                  weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total))
+    gc = ctypes.c_float(0.0)
+    rc = lib().skew_oracle_step_gcoef(ctypes.byref(hp), arr, len(tensors), ctypes.byref(gc))
+    global _LAST_GCOEF
+    _LAST_GCOEF = float(gc.value)
     for k, t in enumerate(tensors):
         t.rms = float(rms[k])
     return rc
+
+
+_LAST_GCOEF = 1.0
+
+
+def last_gcoef() -> float:
+    """The gradient scale of the last ``step`` (1.0 without max_grad_norm)."""
+    return _LAST_GCOEF
 
 
 def bf16_rne(x: np.ndarray) -> np.ndarray:

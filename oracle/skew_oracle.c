@@ -45,6 +45,10 @@ typedef struct {
   float b1, a1, b2, a2, eps, d, lr, s_m, s_0;
   int64_t step;
   uint64_t seed;
+  float wd;       /* lr * lambda, rounded once; 0: no decay */
+  int gclip;      /* gradient-norm scaling on */
+  float gcoef;    /* the gradient scale c (1 when off) */
+  double gc2;     /* c * c, exact in double */
 } consts_t;
 
 static float bf16_bits_to_f32(uint16_t b) {
@@ -136,7 +140,8 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
         double gv = bf16_bits_to_f32(T->g[i * m + j]);
         s += gv * gv;
       }
-      float ri = (float)(s / (double)m);
+      /* with gradient-norm scaling the statistic is c^2 times the exact sum */
+      float ri = (float)((K->gclip ? K->gc2 * s : s) / (double)m);
       T->r[i] = fmaf(K->a2, ri, K->b2 * T->r[i]);
     }
     /* Eq. 1, columns: mean over rows of G*G (each column summed in row order). */
@@ -151,7 +156,7 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
         }
     }
     for (int64_t j = 0; j < m; j++) {
-      float cj = (float)(cs[j] / (double)n);
+      float cj = (float)((K->gclip ? K->gc2 * cs[j] : cs[j]) / (double)n);
       T->c[j] = fmaf(K->a2, cj, K->b2 * T->c[j]);
     }
     free(cs);
@@ -170,7 +175,8 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
     double s = 0.0;
     for (int64_t j = 0; j < m; j++) {
       const int64_t idx = i * m + j;
-      const float g = bf16_bits_to_f32(T->g[idx]);
+      float g = bf16_bits_to_f32(T->g[idx]);
+      if (K->gclip) g = K->gcoef * g;   /* the scaled gradient, rounded once */
       float dd;
       if (exact) {
         T->v[idx] = fmaf(K->a2, g * g, K->b2 * T->v[idx]);
@@ -204,11 +210,14 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
 
   /* dithered bf16 write-back */
   const uint64_t key = skew_oracle_key(K->seed, K->step, T->tensor_id);
+  const int decay = K->wd != 0.0f && T->tier != ORACLE_ROUTER;
 #pragma omp parallel for schedule(static)
   for (int64_t idx = 0; idx < N; idx++) {
     const float w = bf16_bits_to_f32(T->w[idx]);
     const float U = uhat[idx] * kclip;
-    const float x = fmaf(-K->lr, U, w);
+    /* decoupled weight decay, w - (lr lambda) w with one rounding, ahead of the update */
+    const float wdec = decay ? fmaf(-K->wd, w, w) : w;
+    const float x = fmaf(-K->lr, U, wdec);
     const int32_t e = 2 * (int32_t)skew_oracle_u16(key, (uint64_t)idx) + 1 - 65536;
     const float f = (float)e * 0x1p-24f;
     const float y = fmaf(f, fabsf(w), x);
@@ -223,6 +232,10 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
 }
 
 int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n) {
+  return skew_oracle_step_gcoef(hp, t, n, NULL);
+}
+
+int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n, float *gcoef_out) {
   if (hp->step < 1) return -1;
   consts_t K;
   const double b1 = hp->beta1, b2 = hp->beta2, tt = (double)hp->step;
@@ -237,6 +250,26 @@ int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n
   K.s_0 = (float)sqrt(1.0 - pow(b2, tt));
   K.step = hp->step;
   K.seed = hp->seed;
+  K.wd = (float)((double)hp->lr * (double)hp->weight_decay);
+  K.gclip = hp->max_grad_norm > 0.0f;
+  K.gcoef = 1.0f;
+  if (K.gclip) {
+    /* global 2-norm over every element of every tensor, in double, in order */
+    double total = 0.0;
+    for (int i = 0; i < n && hp->gsq_total < 0.0; i++) {
+      const int64_t N = t[i].rows * t[i].cols;
+      for (int64_t idx = 0; idx < N; idx++) {
+        const double gv = bf16_bits_to_f32(t[i].g[idx]);
+        total += gv * gv;
+      }
+    }
+    if (hp->gsq_total >= 0.0) total = hp->gsq_total;
+    double c = (double)hp->max_grad_norm / (sqrt(total) + 1e-6);
+    if (c > 1.0) c = 1.0;   /* NaN stays NaN */
+    K.gcoef = (float)c;
+  }
+  K.gc2 = (double)K.gcoef * (double)K.gcoef;
+  if (gcoef_out) *gcoef_out = K.gcoef;
   for (int i = 0; i < n; i++) step_tensor(&K, &t[i]);
   return 0;
 }

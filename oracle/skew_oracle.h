@@ -41,10 +41,18 @@ typedef struct {
   float lr, beta1, beta2, eps, clip_threshold;
   int64_t step;  /* t >= 1 */
   uint64_t seed;
+  float weight_decay;   /* lambda >= 0: decoupled decay in float32 ahead of the dithered cast
+                           (Sec. 3 footnote, Sec. 6); the router tier takes none (Table 5) */
+  float max_grad_norm;  /* > 0: the gradients of all n tensors are first scaled by
+                           min(1, max_grad_norm / (||G||_2 + 1e-6)) (Sec. 4); 0: off */
+  double gsq_total;     /* < 0: ||G||_2^2 is summed over the n tensors given; >= 0: its value
+                           (a step over a sample of a larger set passes the set's sum) */
 } skew_oracle_hparams;
 
-/* One step over n tensors. Returns 0, or -1 when step < 1. */
+/* One step over n tensors. Returns 0, or -1 when step < 1. When gcoef_out is not NULL it
+ * receives the gradient scale of the step (1 without max_grad_norm). */
 int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n);
+int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n, float *gcoef_out);
 
 /* Pieces exposed for pinning. */
 uint16_t skew_oracle_f32_to_bf16(float f);

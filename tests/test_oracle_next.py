@@ -1,0 +1,229 @@
+"""Pins of the oracle's two optional terms of the step.
+
+Decoupled weight decay (Sec. 3 footnote and Sec. 6: fused into the float32 update ahead of
+the dithered cast; Table 5: lambda = 0.05, none on the router) and the global gradient-norm
+scaling the trainer applies before every step (Sec. 4: clipping at 1.0), both against
+torch's own routines in float64: torch.optim.AdamW for the decay, and
+torch.nn.utils.clip_grad_norm_ followed by torch.optim.Adam for the scaling.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+B, E, R = oracle.BACKBONE, oracle.EXPERT, oracle.ROUTER
+LR, B1, B2, EPS = (float(np.float32(v)) for v in (3e-4, 0.9, 0.999, 1e-8))
+
+
+def bf16(x) -> np.ndarray:
+    t = torch.as_tensor(np.asarray(x, np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def f32(b) -> np.ndarray:
+    return oracle.bf16_to_f32(b)
+
+
+def make(tier, w, tid=0):
+    w = np.ascontiguousarray(w, np.uint16)
+    return oracle.Tensor(tier=tier, w=w.copy(), g=np.zeros_like(w), tensor_id=tid).init_state()
+
+
+def rank1_grads(rng, n, m, steps):
+    a = rng.choice([1.0, 1.5], n) * 2.0 ** rng.integers(-3, 1, n)
+    b = rng.choice([1.0, 1.5], m) * 2.0 ** rng.integers(-3, 1, m)
+    out = []
+    for _ in range(steps):
+        lt = rng.choice([1.0, 1.25, 1.5]) * 2.0 ** -2
+        g = rng.choice([-1.0, 1.0], (n, m)) * np.outer(a, b) * lt
+        out.append(bf16(g))
+    return out
+
+
+# ----------------------------------------------------------------------------- weight decay
+def _adamw_reference(tier, shape, grads, beta1, lam, decayed=True):
+    """torch.optim.AdamW in float64 beside the oracle (eps -> 0, no update clip): the
+    weight the oracle hands to the dither equals AdamW's updated weight."""
+    rng = np.random.default_rng(11)
+    T = make(tier, bf16(rng.normal(0, 0.02, shape)), 3)
+    p = torch.zeros(shape, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=LR, betas=(beta1, B2), eps=0.0, weight_decay=lam if decayed else 0.0,
+                            foreach=False)
+    for t, g in enumerate(grads, start=1):
+        T.g = g
+        w_before = f32(T.w).astype(np.float64)
+        with torch.no_grad():
+            p.copy_(torch.from_numpy(w_before))
+        p.grad = torch.from_numpy(f32(g).astype(np.float64))
+        opt.step()
+        oracle.step([T], t, eps=1e-30, clip_threshold=float("inf"), want_x=True, weight_decay=lam)
+        ref = p.detach().numpy()
+        # two float32 roundings of a value ~|w| (the decayed weight, then the update)
+        np.testing.assert_allclose(T.x_out, ref, rtol=2.5e-7, atol=2e-9)
+
+
+@pytest.mark.parametrize("lam", [0.05, 10.0])
+def test_decay_backbone_vector_is_adamw(lam):
+    rng = np.random.default_rng(12)
+    grads = [bf16(rng.normal(0, 1e-2, (33,)) + 1e-4) for _ in range(6)]
+    _adamw_reference(B, (33,), grads, beta1=B1, lam=lam)
+
+
+@pytest.mark.parametrize("lam", [0.05, 10.0])
+def test_decay_rank_one_expert_is_adamw_without_momentum(lam):
+    rng = np.random.default_rng(13)
+    _adamw_reference(E, (6, 11), rank1_grads(rng, 6, 11, 6), beta1=0.0, lam=lam)
+
+
+def test_router_takes_no_decay():
+    rng = np.random.default_rng(14)
+    grads = [bf16(rng.normal(0, 1e-2, (9, 13)) + 1e-4) for _ in range(4)]
+    _adamw_reference(R, (9, 13), grads, beta1=0.0, lam=10.0, decayed=False)
+
+
+def test_decay_with_zero_update_is_one_rounding():
+    """With U = 0 the weight handed to the dither is RN(w - (lr lambda) w): within half a
+    float ulp of the float64 product, and the router keeps w exactly."""
+    rng = np.random.default_rng(15)
+    w0 = bf16(rng.normal(0, 0.02, (8, 16)))
+    lam = 0.05
+    wd = np.float32(LR * lam)
+    for tier in (B, E, R):
+        T = make(tier, w0)      # zero gradients: R = C = 0, D = sqrt(eps), U = 0
+        oracle.step([T], 1, want_x=True, want_u=True, weight_decay=lam)
+        assert not np.any(T.u_out)
+        w = f32(w0).astype(np.float64)
+        if tier == R:
+            assert np.array_equal(T.x_out, f32(w0))
+        else:
+            exact = w - float(wd) * w
+            ulp = np.spacing(np.abs(exact).astype(np.float32)).astype(np.float64)
+            assert np.all(np.abs(T.x_out.astype(np.float64) - exact) <= 0.5 * ulp)
+            assert np.any(T.x_out != f32(w0))
+
+
+def test_zero_decay_is_bit_identical_to_no_decay():
+    rng = np.random.default_rng(16)
+    w0 = bf16(rng.normal(0, 0.02, (7, 9)))
+    g = bf16(rng.normal(0, 1e-3, (7, 9)))
+    outs = []
+    for lam in (None, 0.0):
+        T = make(B, w0)
+        T.g = g
+        if lam is None:
+            oracle.step([T], 1)
+        else:
+            oracle.step([T], 1, weight_decay=lam)
+        outs.append(T.w.copy())
+    assert np.array_equal(outs[0], outs[1])
+
+
+# ----------------------------------------------------------------------------- gradient norm
+def _clip_adam_reference(specs, steps, max_norm, seed=21):
+    """torch.nn.utils.clip_grad_norm_ over all tensors, then torch.optim.Adam (beta1 = 0 for
+    tiers without momentum), in float64, beside one oracle step over the same tensors."""
+    rng = np.random.default_rng(seed)
+    Ts, ps, opts = [], [], []
+    for k, (tier, shape, grad_fn) in enumerate(specs):
+        Ts.append(make(tier, bf16(rng.normal(0, 0.02, shape)), k))
+        ps.append(torch.zeros(shape, dtype=torch.float64, requires_grad=True))
+        opts.append(torch.optim.Adam([ps[-1]], lr=LR, betas=(B1 if tier == B else 0.0, B2), eps=0.0,
+                                     foreach=False))
+    for t in range(1, steps + 1):
+        for (tier, shape, grad_fn), T, p in zip(specs, Ts, ps):
+            T.g = grad_fn(rng)
+            with torch.no_grad():
+                p.copy_(torch.from_numpy(f32(T.w).astype(np.float64)))
+            p.grad = torch.from_numpy(f32(T.g).astype(np.float64))
+        total = torch.nn.utils.clip_grad_norm_(ps, max_norm)
+        for opt in opts:
+            opt.step()
+        oracle.step(Ts, t, eps=1e-30, clip_threshold=float("inf"), want_x=True, max_grad_norm=max_norm)
+        coef = min(1.0, max_norm / (float(total) + 1e-6))
+        assert abs(oracle.last_gcoef() - coef) <= 1e-7 * coef
+        for T, p in zip(Ts, ps):
+            np.testing.assert_allclose(T.x_out, p.detach().numpy(), rtol=2e-7, atol=4e-9)
+    return Ts
+
+
+def test_gradnorm_is_global_over_tensors_backbone_vectors():
+    specs = [(B, (33,), lambda r: bf16(r.normal(0, 0.3, (33,)) + 1e-3)),
+             (B, (17,), lambda r: bf16(r.normal(0, 0.05, (17,)) + 1e-3))]
+    _clip_adam_reference(specs, 5, max_norm=1.0)
+
+
+def test_gradnorm_router_and_rank_one_matrices():
+    rng = np.random.default_rng(22)
+    g_bb = iter(rank1_grads(rng, 12, 5, 4))
+    specs = [(R, (9, 13), lambda r: bf16(r.normal(0, 0.2, (9, 13)) + 1e-3)),
+             (B, (12, 5), lambda r: next(g_bb))]
+    _clip_adam_reference(specs, 4, max_norm=0.5)
+
+
+def test_gradnorm_above_the_norm_is_bit_identical_to_off():
+    rng = np.random.default_rng(23)
+    shapes = [(8, 24), (40,), (5, 3)]
+    w0 = [bf16(rng.normal(0, 0.02, s)) for s in shapes]
+    g = [bf16(rng.normal(0, 1e-3, s)) for s in shapes]
+    res = []
+    for mgn in (0.0, 1e3):
+        Ts = [make(tier, w) for tier, w in zip((E, B, R), w0)]
+        for T, gg in zip(Ts, g):
+            T.g = gg
+        oracle.step(Ts, 1, max_grad_norm=mgn)
+        assert oracle.last_gcoef() == 1.0
+        res.append([T.w.copy() for T in Ts] + [T.r for T in Ts if T.r is not None])
+    for a, b in zip(*res):
+        assert np.array_equal(a, b)
+
+
+def test_gradnorm_factored_rank_one_equals_exact_tier():
+    """I1 with the scaling on: for rank-one G*G the factored statistics (c^2 times the exact
+    sums) and the exact second moment of the scaled gradient give the same update."""
+    rng = np.random.default_rng(24)
+    n, m = 6, 10
+    w0 = bf16(rng.normal(0, 0.02, (n, m)))
+    Tf, Tx = make(E, w0, 5), make(R, w0, 5)
+    for t, g in enumerate(rank1_grads(rng, n, m, 5), start=1):
+        Tf.g = Tx.g = g
+        oracle.step([Tf], t, want_u=True, max_grad_norm=0.3, gsq_total=float(np.sum(f32(g).astype(np.float64) ** 2)))
+        cf = oracle.last_gcoef()
+        oracle.step([Tx], t, want_u=True, max_grad_norm=0.3)
+        assert oracle.last_gcoef() == cf < 1.0
+        np.testing.assert_allclose(Tf.u_out, Tx.u_out, rtol=2e-6, atol=1e-7)
+
+
+def test_gradnorm_sample_with_the_set_sum_equals_the_full_set():
+    """A step over a sample of the tensors, given the whole set's sum of squares, updates the
+    sample exactly as the step over the whole set does."""
+    rng = np.random.default_rng(25)
+    shapes = [(8, 24), (40,), (5, 3), (16, 16)]
+    tiers = (E, B, R, B)
+    w0 = [bf16(rng.normal(0, 0.02, s)) for s in shapes]
+    g = [bf16(rng.normal(0, 0.1, s)) for s in shapes]
+    full = [make(tier, w) for tier, w in zip(tiers, w0)]
+    for T, gg in zip(full, g):
+        T.g = gg
+    oracle.step(full, 1, max_grad_norm=1.0)
+    c_full = oracle.last_gcoef()
+    assert c_full < 1.0
+    total = sum(float(np.sum(f32(gg).astype(np.float64) ** 2)) for gg in g)
+    part = [make(tiers[i], w0[i]) for i in (0, 3)]
+    for T, i in zip(part, (0, 3)):
+        T.g = g[i]
+    oracle.step(part, 1, max_grad_norm=1.0, gsq_total=total)
+    assert oracle.last_gcoef() == c_full
+    for T, i in zip(part, (0, 3)):
+        assert np.array_equal(T.w, full[i].w)
+
+
+def test_gradnorm_nonfinite_norm_propagates():
+    T = make(E, bf16(np.full((3, 4), 0.01)))
+    g = np.zeros((3, 4), np.float32)
+    g[1, 2] = np.inf
+    T.g = bf16(g)
+    oracle.step([T], 1, max_grad_norm=1.0)
+    # inf norm: the scale is 0 and inf * 0 is NaN
+    assert oracle.last_gcoef() == 0.0
+    assert np.isnan(f32(T.w)).any()

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define SKEW_ABI_VERSION 1
+#define SKEW_ABI_VERSION 2
 
 enum {
   SKEW_OK = 0,
@@ -93,7 +93,16 @@ typedef struct skew_tensor_desc {
  *                   recomputed only when a faster estimate cannot decide its rounding).
  *   step            t >= 1, the caller's step counter (the library keeps none).
  *   seed            dither seed; with (step, tensor_id, element index) it fixes
- *                   every dither value, so results are bit-reproducible. */
+ *                   every dither value, so results are bit-reproducible.
+ *   weight_decay    lambda >= 0 (finite): decoupled weight decay fused into the float32
+ *                   update ahead of the dithered cast, x = fma(-lr, U, w - (lr lambda) w),
+ *                   with lr*lambda rounded once to float (Sec. 3 footnote, Sec. 6; Table 5:
+ *                   0.05). The router tier takes none. 0: off, bit-identical to no decay.
+ *   max_grad_norm   >= 0 (finite); > 0 scales every gradient of the table by
+ *                   c = min(1, max_grad_norm / (||G||_2 + 1e-6)), the norm taken over all
+ *                   tensors of the table (the trainer's clipping at 1.0, Sec. 4), before
+ *                   the step: elementwise terms use fl(c g), the factored statistics c^2
+ *                   times the exact sums of g^2. 0: off. */
 typedef struct skew_hparams {
   float lr;
   float beta1;
@@ -103,6 +112,8 @@ typedef struct skew_hparams {
   int32_t flags;
   int64_t step;
   uint64_t seed;
+  float weight_decay;
+  float max_grad_norm;
 } skew_hparams;
 
 typedef struct skew_ctx skew_ctx;

@@ -13,10 +13,11 @@
 using namespace skew;
 
 namespace {
-constexpr int kLaunches = 9;
+constexpr int kLaunches = 10;
 const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_stats_momentum", "p1_rowcol_sumsq",
                                              "fold_rc_ema", "p2_update_sumsq", "clip_factor",
-                                             "recheck_update_sumsq", "clip_factor_recheck", "p3_apply_dither"};
+                                             "recheck_update_sumsq", "clip_factor_recheck", "p3_apply_dither",
+                                             "grad_norm"};
 }  // namespace
 
 // an item list with the bounds of each pipeline group in it
@@ -32,7 +33,8 @@ struct skew_ctx {
   char *ws = nullptr;   // workspace base (device)
   DevTensor *d_table = nullptr;
   RecheckLists *lists = nullptr;
-  GroupedList p1, fold, p2, p3, clip;
+  GroupedList p1, fold, p2, p3, clip, fold_rows;
+  float *gscale = nullptr;   // device: the gradient-norm mode's scale
   GroupedList z[kZVariants];   // row-band pass items, one list per kernel variant
   hipStream_t side = nullptr;  // the update pass of the pipeline runs here
   std::vector<hipEvent_t> sync;   // [0]: step start, [1]: update pass done, [2 + g]: group g ready
@@ -75,6 +77,9 @@ StepConsts make_consts(const skew_hparams &hp) {
   k.step = hp.step;
   k.seed = hp.seed;
   k.flags = hp.flags;
+  k.wd = (float)((double)hp.lr * (double)hp.weight_decay);
+  k.max_grad_norm = hp.max_grad_norm;
+  k.gclip = hp.max_grad_norm > 0.0f ? 1 : 0;
   return k;
 }
 
@@ -86,6 +91,8 @@ bool hparams_ok(const skew_hparams *hp) {
   if (!(hp->beta2 >= 0.0f && hp->beta2 < 1.0f)) return false;
   if (!(hp->eps > 0.0f) || !std::isfinite(hp->eps)) return false;
   if (!(hp->clip_threshold > 0.0f)) return false;  // +inf allowed: no clipping
+  if (!(hp->weight_decay >= 0.0f) || !std::isfinite(hp->weight_decay)) return false;
+  if (!(hp->max_grad_norm >= 0.0f) || !std::isfinite(hp->max_grad_norm)) return false;
   return true;
 }
 
@@ -175,6 +182,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.nfr = tp.nfr;
     x.nfc = tp.nfc;
     x.kind = tp.kind;
+    x.decay = tp.tier != SKEW_TIER_ROUTER ? 1 : 0;
     x.momentum = tp.momentum;
     x.vec = aligned16(d[i].w) && aligned16(d[i].g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
     x.tensor_id = d[i].tensor_id;
@@ -194,7 +202,8 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   c->lists = reinterpret_cast<RecheckLists *>(ws + p.off_lists);
   Item *const base = reinterpret_cast<Item *>(ws + p.off_items);
   std::vector<Item> items;
-  items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() + 1);
+  items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() +
+                p.fold_rows.size() + 1);
   auto add = [&](GroupedList &gl, const std::vector<Item> &v) {
     gl.d = base + items.size();
     gl.bound.assign((size_t)p.ngroups + 1, 0);
@@ -208,7 +217,9 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   add(c->p2, p.p2);
   add(c->p3, p.p3);
   add(c->clip, p.clip);
+  add(c->fold_rows, p.fold_rows);
   if (items.empty()) items.push_back({0, 0});
+  c->gscale = reinterpret_cast<float *>(ws + p.off_gscale);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
@@ -237,8 +248,10 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
 
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
-  const StepConsts k = make_consts(*hp);
+  StepConsts k = make_consts(*hp);
+  k.gscale = ctx->gscale;
   const Plan &p = ctx->plan;
+  if (k.gclip && p.ngroups != 1) return SKEW_EINVAL;   // the global norm couples every tensor
   hipStream_t s0 = static_cast<hipStream_t>(stream), s1 = ctx->side;
   std::vector<skew_ctx::Timed> *rec = nullptr;
   if (ctx->ev_used < ctx->ev_steps) {
@@ -266,16 +279,35 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
     e = (int)hipEventRecord(ctx->sync[0], s0);
     if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[0], 0);
   }
+  const int nt = (int)p.t.size();
   for (int g = 0; g < p.ngroups && e == 0; g++) {
     // pass 1, fold and clip stage of group g on the caller's stream
-    for (int v = 0; v < kZVariants; v++)
-      if (ctx->z[v].count(g) > 0)
-        run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, s0); });
-    if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
-    if (ctx->fold.count(g) > 0) run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, s0); });
+    if (!k.gclip) {
+      for (int v = 0; v < kZVariants; v++)
+        if (ctx->z[v].count(g) > 0)
+          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 0, s0); });
+      if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
+      if (ctx->fold.count(g) > 0)
+        run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, 0, s0); });
+    } else {
+      // gradient-norm mode (one group): the scale needs every tensor's sum of g^2 before
+      // any statistic, so the row-band pass runs twice: sums, then z with R folded
+      for (int v = 0; v < kZVariants; v++)
+        if (ctx->z[v].count(g) > 0)
+          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 1, s0); });
+      if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
+      if (ctx->p2.count(g) > 0) run(9, s0, [&] { return launch_gsq(T, ctx->p2.at(g), ctx->p2.count(g), s0); });
+      run(9, s0, [&] { return launch_gnorm(T, nt, k, s0); });
+      if (ctx->fold_rows.count(g) > 0)
+        run(3, s0, [&] { return launch_fold(T, ctx->fold_rows.at(g), ctx->fold_rows.count(g), k, 1, s0); });
+      for (int v = 0; v < kZVariants; v++)
+        if (ctx->z[v].count(g) > 0)
+          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 2, s0); });
+      if (ctx->fold.count(g) > 0)
+        run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, 2, s0); });
+    }
     if (ctx->p2.count(g) > 0) run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
     if (ctx->clip.count(g) > 0) {
-      const int nt = (int)p.t.size();
       RecheckLists *L = ctx->lists;
       run(5, s0, [&] { return launch_clip(T, ctx->clip.at(g), ctx->clip.count(g), k, L, nt, s0); });
       // re-checks of the tensors the clip stage listed (launches with empty lists exit at once)
@@ -311,7 +343,7 @@ int skew_timing_enable(skew_ctx *ctx, int max_steps) {
   ctx->ev_steps = ctx->ev_used = 0;
   ctx->ev_next = 0;
   // at most one launch of each kind per group and step (the row-band variants share two kinds)
-  const size_t per_step = (size_t)ctx->plan.ngroups * (kLaunches + kZVariants + 2) * 2;
+  const size_t per_step = (size_t)ctx->plan.ngroups * (kLaunches + 2 * kZVariants + 8) * 2;
   const size_t n = (size_t)max_steps * per_step;
   ctx->ev_pool.reserve(n);
   for (size_t i = 0; i < n; i++) {

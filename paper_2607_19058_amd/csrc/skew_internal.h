@@ -97,7 +97,8 @@ struct DevTensor {
   double *rowpart;        // [ntc][n]   partial row sums of g^2, one per column strip
   double *colpart;        // [ntr][m]   partial column sums of g^2, one per row band (row-band pass: [nzb][m])
   double *ainv;           // [n]        1/sqrt(R_i) after the step's EMA
-  double *rsum;           // [nfr]      sums of R_i over each fold chunk of rows
+  double *rsum;           // [nfr]      sums of R_i over each fold chunk of rows (row-band
+                          //            tensors: [ceil(n / kFold)], in the gradient-norm mode)
   double *zpart;          // [nzb][m]   row-band pass: partial column sums of (s x)^2 / R_i
   BandStats *bst;         // [nzb]      row-band pass: per band
   ColStats *cst;          // [nfc]      row-band pass: per fold chunk of columns
@@ -120,7 +121,7 @@ struct DevTensor {
                           // is wpr = ceil(zcw / nseg) waves, wave w of it takes chunks w, w + wpr
   int32_t nzb;            // row-band pass: row bands
   int32_t zrb;            // row-band pass: rows per group and block
-  int32_t pad2;
+  int32_t decay;          // the decoupled weight decay applies (every tier but the router)
   int64_t zrows;          // row-band pass: rows per band
   uint64_t tensor_id;
 };
@@ -136,6 +137,11 @@ struct StepConsts {
   int32_t flags;   // SKEW_FLAG_*
   int64_t step;
   uint64_t seed;
+  float wd;                 // lr * lambda of the decoupled weight decay, rounded once (0: off)
+  float max_grad_norm;      // > 0: gradients scaled by the global norm's factor
+  int32_t gclip;            // max_grad_norm > 0
+  int32_t pad;
+  float *gscale;            // device: the factor c (written by the norm stage)
 };
 
 // Host-side plan of a descriptor table.
@@ -167,7 +173,11 @@ struct Plan {
   std::vector<TensorPlan> t;
   size_t off_lists = 0;                       // workspace offset of the RecheckLists
   size_t off_zero = 0;                        // workspace offset of 256 zero bytes
+  size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
+  // fold items of the gradient-norm mode's first fold: rows and columns of every factored
+  // tensor (row-band tensors: rows [0, ceil(n / kFold)), then columns)
+  std::vector<Item> fold_rows;
   std::vector<Item> z;                        // row-band pass items (split by kernel variant at init)
   int32_t ngroups = 1;
   std::vector<int32_t> tgroup;                // group of each tensor (item lists are in tensor order)
@@ -184,9 +194,18 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out);
 // Kernel launchers (skew_kernels.hip). Return a hipError_t value.
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream);
 // row-band pass, kernel variant log2(nseg) * 4 + (element loads ? 2 : 0) + (momentum ? 1 : 0)
-int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, void *stream);
+// mode 0: the whole pass; 1: sums of g^2 only (row sums to ainv); 2: z, floored sum and
+// band statistics from the R already folded (the gradient-norm mode's two passes)
+int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, int mode,
+               void *stream);
 
-int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
+// fold phase 0: the step without gradient-norm scaling; 1: its first fold (R and C of every
+// factored tensor from the sums of g^2, scaled by c^2); 2: its second fold (row-band tensors:
+// c' and sum_j z_j / c'_j)
+int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int phase, void *stream);
+// gradient-norm mode: sums of g^2 of exact tensors over the update-sum items, then the scale
+int launch_gsq(const DevTensor *T, const Item *items, int64_t count, void *stream);
+int launch_gnorm(const DevTensor *T, int ntensors, const StepConsts &k, void *stream);
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
               void *stream);

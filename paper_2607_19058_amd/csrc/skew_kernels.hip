@@ -515,9 +515,9 @@ __device__ __forceinline__ double rsq_d(double x) {
 }
 
 template <int NSEG, int RB, bool MOM, bool VEC>
-__device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, unsigned char *bufA,
-                                         unsigned char *bufB, float *rbA, float *rbB, double *rowsh, double *sh,
-                                         float *rstash, const unsigned char *zlds) {
+__device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, int mode,
+                                         unsigned char *bufA, unsigned char *bufB, float *rbA, float *rbB,
+                                         double *rowsh, double *sh, float *rstash, const unsigned char *zlds) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
@@ -559,6 +559,11 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
     for (int e = 0; e < 8; e++) cacc[s][e] = zacc[s][e] = 0.0;
   double ysum = 0.0, ysum2 = 0.0, umax = 0.0;   // the floored sum in two chains
+  // mode 1 (sums only): the band's sum of g^2, kept by lane b * P of each group's first wave
+  double rs_l = 0.0;
+  // mode 2: the gradient scale of the gradient-norm mode (elements enter as fl(c g))
+  const bool scaled = mode == 2;
+  const float gc = scaled ? ldg(k.gscale) : 1.f;
   // a row with R_i == 0 but a nonzero sum (flagged by lane b * P of the group's first wave)
   int bad_l = 0;
 
@@ -635,8 +640,8 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     const int64_t rbase = r0 + blk * br;
     double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
     // row and column sums of g^2 (bf16 squares are exact in double); an idle wave's
-    // accumulators are never used
-    {
+    // accumulators are never used. Mode 2 has them from the first pass.
+    if (mode != 2) {
       double rp[RB];
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
@@ -678,8 +683,21 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     __builtin_amdgcn_s_barrier();
     // R_i after the EMA (Eq. 1) for the group's rb rows, lane-parallel: lane b * P + w
     // takes the partial of wave w of row b; after the segment sum lane b * P holds the row
-    double winv_l;
-    {
+    double winv_l = 0.0;
+    if (mode == 2) {
+      // R_i folded this step (staged with the block)
+      const int b = lane / P, w = lane - b * P;
+      const int r = grp_c * rb + (b < rb ? b : 0);
+      const int64_t i = rbase + r;
+      const float R = rcur[r];
+      const double Rd = (double)R;
+      const bool normal = R > 0.f && R < __builtin_inff();
+      winv_l = (R > 0.f && i < r1) ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
+      if (active && wg == 0 && b < rb && w == 0 && i < r1) {
+        rstash[i - r0] = R;
+        if (R != R) bad_l = 1;
+      }
+    } else {
       const int b = lane / P, w = lane - b * P;
       const int r = grp_c * rb + (b < rb ? b : 0);
       double x = (active && b < rb && w < wpr) ? slot[r * kZWaves + w] : 0.0;
@@ -687,6 +705,13 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       if (P >= 4) x += dpp_d<kDppXor2>(x);
       if (P >= 8) x += dpp_d<kDppHalfMirror>(x);
       const int64_t i = rbase + r;
+      if (mode == 1) {
+        // the row's sum of g^2: R is folded once the gradient scale is known
+        if (active && wg == 0 && b < rb && w == 0 && i < r1) {
+          stg(t.ainv + i, x);
+          rs_l += x;
+        }
+      } else {
       const float ri = div_to_float(x, dm, rdm);
       const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, rcur[r]));
       const double Rd = (double)R;
@@ -697,6 +722,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         // wait for its staged rows until the store completes
         rstash[i - r0] = R;
         if (R != R || (!(R > 0.f) && x > 0.0)) bad_l = 1;
+      }
       }
     }
     // z_j, the floored sum and the bound (the sums the prediction asks for)
@@ -720,6 +746,10 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
           __builtin_amdgcn_sched_barrier(0);
           float x[8];
           unpack8(u[bb][s], x);
+          if (scaled) {
+#pragma unroll
+            for (int e = 0; e < 8; e++) x[e] = gc * x[e];
+          }
           if (MOM) {
             const unsigned char *mp =
                 (chs[s] < zcw ? cur + goff_m + (size_t)(r * zcw + chs[s]) * 2048 : zlds) + lane * 32;
@@ -751,12 +781,14 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
           }
         }
         if (Z) umax = fmax(umax, ((double)amax * (double)amax) * winv);
+        // a row with R_i == 0 but nonzero elements (mode 0 tests its sum instead)
+        if (Z && scaled && winv == 0.0 && amax > 0.f) bad_l = 1;
       }
       }
       __builtin_amdgcn_sched_barrier(0);
     };
-    if (!active)
-      ;   // an idle wave (its rows are group 0's) adds nothing
+    if (!active || mode == 1)
+      ;   // an idle wave (its rows are group 0's) adds nothing; mode 1 forms no update sums
     else if (want_z && want_y)
       sweep2(std::true_type(), std::true_type());
     else if (want_z)
@@ -806,22 +838,25 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
       for (int e = 0; e < 8; e++) {
         if (VEC || col[s] + e < m) {
-          stg(t.colpart + prow + col[s] + e, cacc[s][e]);
-          stg(t.zpart + prow + col[s] + e, zacc[s][e]);
+          if (mode != 2) stg(t.colpart + prow + col[s] + e, cacc[s][e]);
+          if (mode != 1) stg(t.zpart + prow + col[s] + e, zacc[s][e]);
         }
       }
     }
   }
   // the band's R and 1/sqrt(R) (coalesced), and its statistics: fixed-order reductions
+  // (mode 1: the band's sum of g^2 instead; mode 2: R was written by the fold)
   const int64_t nrows = r1 - r0;
-  double rs = 0.0;
+  double rs = rs_l;
   float rmn = __builtin_inff(), rmx = 0.f;
-  for (int64_t j = threadIdx.x; j < nrows; j += kZThreads) {
+  for (int64_t j = threadIdx.x; mode != 1 && j < nrows; j += kZThreads) {
     const float R = rstash[j];
     const double Rd = (double)R;
     const bool normal = R > 0.f && R < __builtin_inff();
-    stg(t.R + r0 + j, R);
-    stg(t.ainv + r0 + j, normal ? rsq_d(Rd) : 1.0 / sqrt(Rd));
+    if (mode == 0) {
+      stg(t.R + r0 + j, R);
+      stg(t.ainv + r0 + j, normal ? rsq_d(Rd) : 1.0 / sqrt(Rd));
+    }
     rs += Rd;
     if (R > 0.f) rmn = fminf(rmn, R);
     rmx = fmaxf(rmx, R);
@@ -845,7 +880,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 
 template <int NSEG, bool MOM, bool VEC>
 __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restrict__ TT,
-                                                        const Item *__restrict__ items, StepConsts k) {
+                                                        const Item *__restrict__ items, StepConsts k, int mode) {
   __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes];
   __shared__ __attribute__((aligned(16))) unsigned char bufB[kZLdsBytes];
   __shared__ float rbA[64], rbB[64];
@@ -860,11 +895,11 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
   // and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG <= 2 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
   else
-    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
 }
 
 // fixed-order work-group sum of p[0], p[stride], ..., p[(n-1) stride]: thread j sums
@@ -876,27 +911,38 @@ __device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh,
 }
 // q = max(mean R, eps) for a factored tensor (the clamp of the reconstruction), from the
 // sums of R over the fold chunks of rows or over the row bands
-__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, float eps, double *sh) {
-  const double sr = t.zpath ? wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double))
-                            : wg_sum(t.rsum, t.nfr, sh);
-  return max_nan((float)(sr / (double)t.n), eps);
+__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, const StepConsts &k, double *sh) {
+  // row-band tensors keep the sums of R in their band statistics, except in the gradient-
+  // norm mode, where the fold forms R and its sums per chunk of rows as for wide tensors
+  const double sr = (t.zpath && !k.gclip) ? wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double))
+                                          : wg_sum(t.rsum, t.zpath ? (t.n + kFold - 1) / kFold : t.nfr, sh);
+  return max_nan((float)(sr / (double)t.n), k.eps);
 }
 
 // --------------------------------------------------------------------------------------------
 // fold: R_i <- b2 R_i + a2 r_i, C_j <- b2 C_j + a2 c_j (Eq. 1), 1/sqrt(R_i), sums of R
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restrict__ TT,
-                                                        const Item *__restrict__ items, StepConsts k) {
+                                                        const Item *__restrict__ items, StepConsts k, int phase) {
   __shared__ double sh[kThreads];
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  if (it.tile < t.nfr) {
+  // gradient-norm mode: the statistics of the scaled gradient are c^2 times the exact sums
+  const double c2 = phase == 1 ? (double)ldg(k.gscale) * (double)ldg(k.gscale) : 1.0;
+  // row chunks of this launch: wide tensors always; row-band tensors only in phase 1,
+  // where their row sums of g^2 wait in ainv
+  const int nrows = t.zpath ? (phase == 1 ? (int)((t.n + kFold - 1) / kFold) : 0) : t.nfr;
+  if (phase == 2 && !t.zpath) return;
+  if (it.tile < nrows) {
     const int64_t i = (int64_t)it.tile * kFold + threadIdx.x;
     double rn = 0.0;
     if (i < t.n) {
       double s = 0.0;
-      for (int q = 0; q < t.ntc; q++) s += ldg(t.rowpart + (int64_t)q * t.n + i);
-      const float ri = (float)(s / (double)t.m);
+      if (t.zpath)
+        s = ldg(t.ainv + i);
+      else
+        for (int q = 0; q < t.ntc; q++) s += ldg(t.rowpart + (int64_t)q * t.n + i);
+      const float ri = (float)((phase == 1 ? c2 * s : s) / (double)t.m);
       const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, ldg(t.R + i)));
       stg(t.R + i, R);
       stg(t.ainv + i, 1.0 / sqrt((double)R));
@@ -904,17 +950,20 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     }
     const double tot = block_sum(rn, sh);
     if (threadIdx.x == 0) stg(t.rsum + it.tile, tot);
-  } else if (!t.zpath) {
-    const int64_t j = (int64_t)(it.tile - t.nfr) * kFold + threadIdx.x;
+  } else if (!t.zpath || phase == 1) {
+    // C_j from the column partials ([row bands][m] of either pass 1)
+    const int64_t j = (int64_t)(it.tile - nrows) * kFold + threadIdx.x;
     if (j < t.m) {
       double s = 0.0;
-      for (int b = 0; b < t.ntr; b++) s += ldg(t.colpart + (int64_t)b * t.m + j);
-      const float cj = (float)(s / (double)t.n);
+      const int nb = t.zpath ? t.nzb : t.ntr;
+      for (int b = 0; b < nb; b++) s += ldg(t.colpart + (int64_t)b * t.m + j);
+      const float cj = (float)((phase == 1 ? c2 * s : s) / (double)t.n);
       stg(t.C + j, fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j))));
     }
   } else {
-    // row-band tensor: C_j, c'_j = C_j / max(mean R, eps) and sum_j z_j / c'_j over the chunk
-    const float q = mean_r_clamped(t, k.eps, sh);
+    // row-band tensor: C_j (phase 0; phase 2 has it from phase 1), c'_j = C_j / max(mean R,
+    // eps) and sum_j z_j / c'_j over the chunk
+    const float q = mean_r_clamped(t, k, sh);
     const int64_t j = (int64_t)it.tile * kFold + threadIdx.x;
     double sj = 0.0;
     float cmn = __builtin_inff(), cmx = 0.f;
@@ -925,9 +974,14 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
         cs += ldg(t.colpart + (int64_t)p * t.m + j);
         zs += ldg(t.zpart + (int64_t)p * t.m + j);
       }
-      const float cj = (float)(cs / (double)t.n);
-      const float C = fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j)));
-      stg(t.C + j, C);
+      float C;
+      if (phase == 0) {
+        const float cj = (float)(cs / (double)t.n);
+        C = fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j)));
+        stg(t.C + j, C);
+      } else {
+        C = ldg(t.C + j);
+      }
       const float cp = C / q;
       if (C > 0.f) {
         // c'_j that is zero or not finite leaves the tensor to the exact pass
@@ -951,6 +1005,56 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
       stg(&t.cst[it.tile].cmax, cmax);
       stg(&t.cst[it.tile].bad, b);
     }
+  }
+}
+
+// Gradient-norm mode: sum of g^2 of each (tile, part) of an exact tensor, into its update-sum
+// slot (the update-sum pass later overwrites it); factored items have theirs in pass 1
+__global__ __launch_bounds__(kThreads) void gsq_kernel(const DevTensor *__restrict__ TT,
+                                                       const Item *__restrict__ items) {
+  __shared__ double sh[kThreads];
+  const Item it = items[blockIdx.x];   // it.tile = tile * kSub + part
+  const DevTensor &t = TT[it.tensor];
+  if (t.kind == kFactored) return;
+  const Tile tl = tile_of(t, it.tile / kSub);
+  const WaveMap wm(t, tl);
+  const int64_t r0 = wm.wr + (int64_t)(it.tile % kSub) * wm.rpi, rs = (int64_t)wm.rpi * kSub;
+  double acc = 0.0;
+  for (int64_t lr = r0; lr < tl.nr; lr += rs) {
+    const int64_t i = tl.row(lr);
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+      if (wm.col + e >= t.m) continue;
+      const double g = (double)bf_one(ldg(t.g + i * t.ld + wm.col + e));
+      acc += g * g;
+    }
+  }
+  const double s = block_sum(acc, sh);
+  if (threadIdx.x == 0) stg(t.ssum + it.tile, s);
+}
+
+// Gradient-norm mode: ||G||^2 over every tensor of the table in table order, then the scale
+// c = min(1, max_grad_norm / (||G|| + 1e-6)) (NaN propagates). One work-group.
+__global__ __launch_bounds__(kThreads) void gnorm_kernel(const DevTensor *__restrict__ TT, int ntensors,
+                                                         StepConsts k) {
+  __shared__ double sh[kThreads];
+  double total = 0.0;
+  for (int i = 0; i < ntensors; i++) {
+    const DevTensor &t = TT[i];
+    if (t.n * t.m == 0) continue;
+    double s;
+    if (t.kind != kFactored)
+      s = wg_sum(t.ssum, (int64_t)t.ntr * t.ntc * kSub, sh);
+    else if (t.zpath)
+      s = wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double));
+    else
+      s = wg_sum(t.rowpart, (int64_t)t.ntc * t.n, sh);
+    total += s;
+  }
+  if (threadIdx.x == 0) {
+    double c = (double)k.max_grad_norm / (sqrt(total) + 1e-6);
+    if (c > 1.0) c = 1.0;
+    stg(k.gscale, (float)c);
   }
 }
 
@@ -987,6 +1091,7 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
   const float s = mom ? k.s_m : k.s_0;
   const float deps = sqrtf(k.eps);                    // the oracle's D on the floor
   const float reps = (float)(1.0 / (double)deps);     // correctly rounded 1/D
+  const float gc = k.gclip ? ldg(k.gscale) : 1.f;     // gradient-norm mode: elements are fl(c g)
   SumPair acc = {0.0, 0.0};
   if (col >= m) return acc;
   float cp[8];    // c'_j = C_j / q, rounded as the oracle
@@ -1023,6 +1128,13 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
       float xa[8], xb[8];
       unpack8(ga, xa);
       unpack8(gb, xb);
+      if (k.gclip) {
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+          xa[e] = gc * xa[e];
+          xb[e] = gc * xb[e];
+        }
+      }
       if (mom) {
 #pragma unroll
         for (int e = 0; e < 8; e++) {
@@ -1052,6 +1164,7 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
       for (int e = 0; e < 8; e++) {
         if (col + e >= m) continue;
         float x = bf_one(ldg(t.g + i * ld + col + e));
+        if (k.gclip) x = gc * x;
         if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
         elem(x, Ri, ai, e, acc);
       }
@@ -1069,6 +1182,7 @@ __device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Ti
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
   const float s = mom ? k.s_m : k.s_0;
+  const float gc = k.gclip ? ldg(k.gscale) : 1.f;
   double acc = 0.0;
   if (col >= m) return 0.0;
   float cp[8];
@@ -1081,6 +1195,7 @@ __device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Ti
     for (int e = 0; e < 8; e++) {
       if (col + e >= m) continue;
       float x = bf_one(ldg(t.g + i * ld + col + e));
+      if (k.gclip) x = gc * x;
       if (mom) x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
       const float u = __fmul_rn(s, x) / sqrtf(max_nan(__fmul_rn(Ri, cp[e]), k.eps));
       acc = fma((double)u, (double)u, acc);
@@ -1095,6 +1210,7 @@ __device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, i
   const int64_t r0 = wm.wr + (int64_t)part * wm.rpi, rs = (int64_t)wm.rpi * kSub;
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
+  const float gc = k.gclip ? ldg(k.gscale) : 1.f;
   double acc = 0.0;
   for (int64_t lr = r0; lr < tl.nr; lr += rs) {
     const int64_t i = tl.row(lr);
@@ -1102,7 +1218,8 @@ __device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, i
     for (int e = 0; e < 8; e++) {
       if (col + e >= m) continue;
       const int64_t sidx = i * m + col + e;
-      const float g = bf_one(ldg(t.g + i * ld + col + e));
+      float g = bf_one(ldg(t.g + i * ld + col + e));
+      if (k.gclip) g = gc * g;
       const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
       const float dd = sqrtf(max_nan(vn, k.eps));
       const float num = mom ? __fmul_rn(k.s_m, fmaf(k.a1, g, __fmul_rn(k.b1, ldg(t.M + sidx)))) : __fmul_rn(k.s_0, g);
@@ -1122,7 +1239,7 @@ __global__ __launch_bounds__(kThreads) void p2_kernel(const DevTensor *__restric
   const int part = it.tile % kSub;
   SumPair acc;
   if (t.kind == kFactored) {
-    const float q = mean_r_clamped(t, k.eps, sh);
+    const float q = mean_r_clamped(t, k, sh);
     acc = p2_factored(t, tl, part, k, q);
   } else {
     acc.s = p2_exact(t, tl, part, k);   // already the oracle's own U_hat
@@ -1169,7 +1286,7 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
     const int tile = (int)(idx - base);   // tile * kSub + part
     const Tile tl = tile_of(t, tile / kSub);
     const int part = tile % kSub;
-    const float q = mean_r_clamped(t, k.eps, sh);
+    const float q = mean_r_clamped(t, k, sh);
     if (level == 1) {
       const SumPair acc = p2_factored(t, tl, part, k, q);
       const double sv = block_sum(acc.s, sh);
@@ -1255,7 +1372,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   const DevTensor &t = TT[it.tensor];
   const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
   const double N = (double)(t.n * t.m);
-  const float q = t.kind == kFactored ? mean_r_clamped(t, k.eps, sh) : 0.f;
+  const float q = t.kind == kFactored ? mean_r_clamped(t, k, sh) : 0.f;
   double S = 0.0, spread = 0.0;
   bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t.kind == kFactored;
   int why = amb ? kWhyForced : 0;
@@ -1336,14 +1453,19 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   }
 }
 
+// The weight the update starts from: w - (lr lambda) w with one rounding when the decoupled
+// weight decay applies (Sec. 3 footnote, Sec. 6), else w itself
+__device__ __forceinline__ float decayed(float w, bool dec, float wd) { return dec ? fmaf(-wd, w, w) : w; }
+
 // The oracle's float sequence for one factored element (Alg. 1 with the eps clamps):
-// D = sqrt(max(R_i * c'_j, eps)), U = ((s * x) / D) * k, y = (w - lr U) + xi.
-__device__ __forceinline__ float exact_factored_y(float x, float w, float Ri, float cpj, float s, float kc,
-                                                  float eps, float lr, float dith) {
+// D = sqrt(max(R_i * c'_j, eps)), U = ((s * x) / D) * k, y = (wd - lr U) + xi, where wd is
+// the (decayed) starting weight and xi scales with the pre-step |w|.
+__device__ __forceinline__ float exact_factored_y(float x, float w, float wd, float Ri, float cpj, float s,
+                                                  float kc, float eps, float lr, float dith) {
   const float vh = __fmul_rn(Ri, cpj);
   const float dd = sqrtf(max_nan(vh, eps));
   const float U = __fmul_rn(__fmul_rn(s, x) / dd, kc);
-  return fmaf(dith, fabsf(w), fmaf(-lr, U, w));
+  return fmaf(dith, fabsf(w), fmaf(-lr, U, wd));
 }
 
 // y may round differently from the oracle's value when this is >= 0: the fast update x*F
@@ -1358,7 +1480,7 @@ __device__ __forceinline__ float boundary_slack(float y, float xF, float w) {
 __device__ __forceinline__ bool near_boundary(float y, float xF, float w) { return boundary_slack(y, xF, w) >= 0.f; }
 
 struct P3Scalars {
-  float q, s, kc, cap3, eps, lr;
+  float q, s, kc, cap3, eps, lr, gc;
   double lsk;
 };
 
@@ -1372,6 +1494,10 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
   float x[8], w[8];
   unpack8(gw, x);
   unpack8(ww, w);
+  if (k.gclip) {
+#pragma unroll
+    for (int e = 0; e < 8; e++) x[e] = c.gc * x[e];
+  }
   if (mom) {
 #pragma unroll
     for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
@@ -1390,11 +1516,12 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
     dith[2 * e2] = dither_lo(h);
     dith[2 * e2 + 1] = dither_hi(h);
   }
+  const bool dec = t.decay && k.wd != 0.f;
   float slack = -1.f;
 #pragma unroll
   for (int e = 0; e < 8; e++) {
     const float F = fminf(alpha * bf[e], c.cap3);
-    y[e] = fmaf(dith[e], fabsf(w[e]), fmaf(-x[e], F, w[e]));
+    y[e] = fmaf(dith[e], fabsf(w[e]), fmaf(-x[e], F, decayed(w[e], dec, k.wd)));
     slack = fmaxf(slack, boundary_slack(y[e], x[e] * F, w[e]));
   }
   if (slack >= 0.f) {
@@ -1403,7 +1530,8 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
     for (int e = 0; e < 8; e++) {
       const float F = fminf(alpha * bf[e], c.cap3);
       if (near_boundary(y[e], x[e] * F, w[e]))
-        y[e] = exact_factored_y(x[e], w[e], Ri, ldg(t.C + col + e) / c.q, c.s, c.kc, c.eps, c.lr, dith[e]);
+        y[e] = exact_factored_y(x[e], w[e], decayed(w[e], dec, k.wd), Ri, ldg(t.C + col + e) / c.q, c.s, c.kc,
+                                c.eps, c.lr, dith[e]);
     }
   }
   stg(reinterpret_cast<uint4 *>(t.w + i * t.ld + col),
@@ -1424,6 +1552,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
   c.eps = k.eps;
   c.lr = k.lr;
   c.lsk = (double)k.lr * (double)c.s * (double)kc;   // lr * s * k
+  c.gc = k.gclip ? ldg(k.gscale) : 1.f;             // gradient-norm mode: elements are fl(c g)
   c.cap3 = (float)(c.lsk / (double)sqrtf(k.eps));
   if (t.vec) {
     float bf[8];
@@ -1454,6 +1583,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         if (col + e >= m) continue;
         float x = bf_one(ldg(t.g + i * ld + col + e));
         const float w = bf_one(ldg(t.w + i * ld + col + e));
+        if (k.gclip) x = c.gc * x;
         if (mom) {
           x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
           stg(t.M + i * m + col + e, x);
@@ -1461,9 +1591,10 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         const uint64_t idx = rowidx + (uint64_t)(col + e);
         const float dith = dither_of(dz.pair(idx >> 1), idx);
         const float F = fminf(alpha * (float)col_factor(t, col + e, c.q), c.cap3);
-        float y = fmaf(dith, fabsf(w), fmaf(-x, F, w));
+        const float wd = decayed(w, t.decay && k.wd != 0.f, k.wd);
+        float y = fmaf(dith, fabsf(w), fmaf(-x, F, wd));
         if (near_boundary(y, x * F, w))
-          y = exact_factored_y(x, w, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith);
+          y = exact_factored_y(x, w, wd, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith);
         stg(t.w + i * ld + col + e, to_bf16(y));
       }
     }
@@ -1476,13 +1607,15 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
   const WaveMap wm(t, tl);
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
+  const float gc = k.gclip ? ldg(k.gscale) : 1.f;
   for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
     const int64_t i = tl.row(lr);
 #pragma unroll
     for (int e = 0; e < 8; e++) {
       if (col + e >= m) continue;
       const int64_t sidx = i * m + col + e;
-      const float g = bf_one(ldg(t.g + i * ld + col + e));
+      float g = bf_one(ldg(t.g + i * ld + col + e));
+      if (k.gclip) g = gc * g;
       const float w = bf_one(ldg(t.w + i * ld + col + e));
       const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
       stg(t.V + sidx, vn);
@@ -1496,7 +1629,7 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
         num = __fmul_rn(k.s_0, g);
       }
       const float U = __fmul_rn(num / dd, kc);
-      const float x = fmaf(-k.lr, U, w);
+      const float x = fmaf(-k.lr, U, decayed(w, t.decay && k.wd != 0.f, k.wd));
       const uint64_t idx = (uint64_t)sidx;
       const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), fabsf(w), x);
       stg(t.w + i * ld + col + e, to_bf16(y));
@@ -1533,13 +1666,14 @@ int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream
   hipLaunchKernelGGL(p1_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items);
   return (int)hipGetLastError();
 }
-int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, void *stream) {
+int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, int mode,
+               void *stream) {
   if (count <= 0) return hipSuccess;
   const dim3 grid((uint32_t)count), block(kZThreads);
   hipStream_t s = (hipStream_t)stream;
   switch (variant) {
 #define SKEW_P1Z_CASE(V, NSEG, VEC, MOM) \
-  case V: hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC>), grid, block, 0, s, T, items, k); break;
+  case V: hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC>), grid, block, 0, s, T, items, k, mode); break;
     SKEW_P1Z_CASE(0, 1, true, false)
     SKEW_P1Z_CASE(1, 1, true, true)
     SKEW_P1Z_CASE(2, 1, false, false)
@@ -1557,9 +1691,18 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
   }
   return (int)hipGetLastError();
 }
-int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
+int launch_fold(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int phase, void *stream) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(fold_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
+  hipLaunchKernelGGL(fold_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, phase);
+  return (int)hipGetLastError();
+}
+int launch_gsq(const DevTensor *T, const Item *items, int64_t count, void *stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gsq_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items);
+  return (int)hipGetLastError();
+}
+int launch_gnorm(const DevTensor *T, int ntensors, const StepConsts &k, void *stream) {
+  hipLaunchKernelGGL(gnorm_kernel, dim3(1), dim3(kThreads), 0, (hipStream_t)stream, T, ntensors, k);
   return (int)hipGetLastError();
 }
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {

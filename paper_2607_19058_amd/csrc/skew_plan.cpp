@@ -99,9 +99,13 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.off_ainv = ws_part; ws_part = align_up(ws_part + (size_t)tp.n * 8);
       tp.off_bst = ws_part; ws_part = align_up(ws_part + (size_t)nzb * sizeof(BandStats));
       tp.off_cst = ws_part; ws_part = align_up(ws_part + (size_t)nfc * sizeof(ColStats));
+      const int64_t nzr = ceil_div(tp.n, kFold);   // row chunks of the gradient-norm mode's fold
+      if (nzr > INT32_MAX / 4) return SKEW_EINVAL;
+      tp.off_rsum = ws_part; ws_part = align_up(ws_part + (size_t)nzr * 8);
       for (int32_t k = 0; k < tp.nzb; k++) p.z.push_back({i, k});
       for (int32_t k = 0; k < tp.nfc; k++) p.fold.push_back({i, k});
-      items_total += nzb + nfc;
+      for (int32_t k = 0; k < (int32_t)nzr + tp.nfc; k++) p.fold_rows.push_back({i, k});
+      items_total += nzb + nfc + nzr + nfc;
     } else if (tp.kind == kFactored) {
       const int64_t nfr = ceil_div(tp.n, kFold), nfc = ceil_div(tp.m, kFold);
       if (nfr + nfc > INT32_MAX / 2) return SKEW_EINVAL;
@@ -113,7 +117,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.off_rsum = ws_part; ws_part = align_up(ws_part + (size_t)nfr * 8);
       for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p1.push_back({i, k});
       for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold.push_back({i, k});
-      items_total += tiles + nfr + nfc;
+      for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold_rows.push_back({i, k});
+      items_total += tiles + 2 * (nfr + nfc);
     }
     if (!tp.zpath) {
       for (int32_t k = 0; k < tp.ntr * tp.ntc * kSub; k++) p.p2.push_back({i, k});   // tile * kSub + part
@@ -151,11 +156,13 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
   p.off_items = ws;
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
-                                     p.clip.size() + 1));
+                                     p.clip.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
   ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(n, 1));
   p.off_zero = ws;   // zero-filled with the workspace at set-up and never written
   ws = align_up(ws + 256);
+  p.off_gscale = ws;
+  ws = align_up(ws + sizeof(float));
   auto shift = [ws](size_t &off) {
     if (off != SIZE_MAX) off += ws;
   };

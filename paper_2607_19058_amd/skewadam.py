@@ -18,7 +18,7 @@ SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
 FLAG_EXACT_CLIP = 1
 TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 # names every build of the library exports (checked by the CPU test suite)
 EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
@@ -46,6 +46,7 @@ class HParams(ctypes.Structure):
         ("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
         ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float), ("flags", ctypes.c_int32),
         ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
+        ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float),
     ]
 
 
@@ -170,8 +171,10 @@ class SkewAdam:
         return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
 
     def step(self, step: int, lr: float = 3e-4, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
-             clip_threshold: float = 1.0, seed: int = 0, stream=None, flags: int = 0) -> None:
-        hp = HParams(lr, beta1, beta2, eps, clip_threshold, int(flags), int(step), int(seed) & (2**64 - 1))
+             clip_threshold: float = 1.0, seed: int = 0, stream=None, flags: int = 0, weight_decay: float = 0.0,
+             max_grad_norm: float = 0.0) -> None:
+        hp = HParams(lr, beta1, beta2, eps, clip_threshold, int(flags), int(step), int(seed) & (2**64 - 1),
+                     weight_decay, max_grad_norm)
         rc = self._lib.skew_step(self._ctx, ctypes.byref(hp), self._stream(stream))
         if rc != SKEW_OK:
             raise SkewError(rc, "skew_step")

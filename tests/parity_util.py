@@ -97,10 +97,15 @@ class ParityRun:
             self.O[k].g = bits(self.G[k])
         torch.cuda.synchronize()
         t0 = time.time()
+        # the gradient-norm scaling couples every tensor: an oracle step over a sample gets the
+        # whole set's sum of squares, formed here on the host from the bf16 bits
+        extra = {}
+        if self.hp.get("max_grad_norm", 0.0) > 0.0 and len(self.sample) < len(self.specs):
+            extra["gsq_total"] = float(sum(float(torch.sum(G.cpu().double() ** 2)) for G in self.G))
         self.opt.step(t, seed=self.seed, flags=self.flags, **self.hp)
         torch.cuda.synchronize()
         t1 = time.time()
-        oracle.step([self.O[k] for k in self.sample], t, seed=self.seed, want_y=True, **self.hp)
+        oracle.step([self.O[k] for k in self.sample], t, seed=self.seed, want_y=True, **self.hp, **extra)
         t2 = time.time()
         st = Stats()
         if check:

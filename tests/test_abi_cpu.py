@@ -26,7 +26,7 @@ def test_library_exports_every_declared_function():
     L = ctypes.CDLL(P.skewadam.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
-    assert P.lib().skew_abi_version() == 1
+    assert P.lib().skew_abi_version() == P.skewadam.ABI_VERSION == 2
     for code in (0, -1, -2, -3, -4, -99):
         assert P.lib().skew_strerror(code)
 

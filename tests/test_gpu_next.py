@@ -1,0 +1,136 @@
+"""GPU parity of the step's two optional terms against the CPU oracle: the decoupled weight
+decay fused ahead of the dithered cast (Sec. 3 footnote, Sec. 6; router exempt) and the
+global gradient-norm scaling (the trainer's clipping at 1.0, Sec. 4), alone and together,
+on the tiny workload (every tensor), the unit shapes, and sampled tensors of the one-layer,
+ragged and 6.78B workloads. The gradient-norm mode runs the row-band pass twice (sums, then
+the update sums with R folded under the scale), so these tests also cover that path."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_19058_amd import SkewAdam
+from paper_2607_19058_amd import workloads as W
+
+from parity_util import log, run
+
+pytestmark = pytest.mark.gpu
+
+DECAY = dict(oracle.DEFAULTS, weight_decay=0.05)
+STRONG_DECAY = dict(oracle.DEFAULTS, weight_decay=10.0)     # lr*lambda = 3e-3: visible in bf16
+GNORM = dict(oracle.DEFAULTS, max_grad_norm=1.0)
+BOTH = dict(oracle.DEFAULTS, weight_decay=0.05, max_grad_norm=1.0)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a HIP device")
+    torch.cuda.init()
+
+
+@pytest.mark.parametrize("hp", [DECAY, STRONG_DECAY], ids=["lambda0.05", "lambda10"])
+def test_decay_tiny_every_tensor(hp):
+    log(f"[parity] tiny, weight decay {hp['weight_decay']}: 21 tensors, 10 steps, all compared")
+    st = run(W.get("tiny"), hp=hp)
+    assert st.ok(), st
+
+
+@pytest.mark.parametrize("hp", [GNORM, BOTH], ids=["gnorm", "gnorm+decay"])
+def test_gradnorm_tiny_every_tensor(hp):
+    log(f"[parity] tiny, gradient norm {hp}: 21 tensors, 10 steps, all compared")
+    st = run(W.get("tiny"), hp=hp)
+    assert st.ok(), st
+
+
+def test_gradnorm_tiny_exact_clip_everywhere():
+    from paper_2607_19058_amd.skewadam import FLAG_EXACT_CLIP
+    log("[parity] tiny, gradient norm and decay, exact clip re-check forced")
+    st = run(W.get("tiny"), hp=BOTH, flags=FLAG_EXACT_CLIP)
+    assert st.ok(), st
+
+
+def _unit_workload():
+    specs = []
+    shapes = [(1, 1), (1, 7), (7, 1), (3, 5), (13, 17), (256, 8), (64, 520), (33, 1031), (5,), (1,), (4097,),
+              (2, 2048), (300, 2056)]
+    for tier in (W.BACKBONE, W.EXPERT, W.ROUTER):
+        for sh in shapes:
+            specs.append(W.Spec(f"t{tier}_{'x'.join(map(str, sh))}", tier, sh, len(specs)))
+    return W.Workload("unit", specs, 3)
+
+
+def test_gradnorm_unit_shapes_all_tiers():
+    log("[parity] unit shapes, gradient norm 0.05 and strong decay, 3 steps")
+    st = run(_unit_workload(), hp=dict(oracle.DEFAULTS, lr=1e-2, weight_decay=2.0, max_grad_norm=0.05))
+    assert st.ok(), st
+
+
+def test_gradnorm_scale_above_the_norm_is_the_plain_step():
+    """A max_grad_norm above ||G|| gives scale 1 and the same bits as the step without it
+    (the two-pass path against the one-pass path)."""
+    dev = torch.device("cuda")
+    wl = W.get("tiny")
+    G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
+    outs = []
+    for mgn in (0.0, 1e4):
+        Wt = [W.init_weight(s, wl, dev) for s in wl.specs]
+        opt = SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+        for t in range(1, 6):
+            sc = W.expert_scales(wl, t)
+            for k, s in enumerate(wl.specs):
+                W.fill_grad(s, wl, t, G[k], sc)
+            opt.step(t, max_grad_norm=mgn)
+        torch.cuda.synchronize()
+        outs.append(([w.clone() for w in Wt], opt.state.clone()))
+        opt.close()
+    for a, b in zip(outs[0][0], outs[1][0]):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert torch.equal(outs[0][1], outs[1][1])
+
+
+def test_gradnorm_layer_sampled():
+    wl = W.get("layer")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sc = W.expert_scales(wl, 1)[0]
+    zero_e = int(np.flatnonzero(sc == 0)[0])
+    big_e = int(np.argmax(sc))
+    sample = [names["attn.0"], names["ffn.down"], names[f"ex{zero_e}.up"], names[f"ex{big_e}.up"],
+              names["ex7.down"], names["router"]]
+    log(f"[parity] layer, gradient norm and decay: 263 tensors, 5 steps, sampled {sample}")
+    st = run(wl, sample=sample, hp=BOTH)
+    assert st.ok(), st
+
+
+def test_gradnorm_ragged_sampled():
+    wl = W.get("ragged")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sample = [names["norm.1"], names["bias.2"], names["attn.0"], names["exA3.up"], names["exB40.down"],
+              names["router"]]
+    log(f"[parity] ragged, gradient norm and decay: 269 tensors, 8 steps, sampled {sample}")
+    st = run(wl, steps=8, sample=sample, hp=BOTH)
+    assert st.ok(), st
+
+
+def test_gradnorm_full_6p78b_sampled():
+    wl = W.get("full")
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sample = [names["norm.3"], names["attn.7"], names["lm_head"], names["ex5.gate"], names["ex77.down"],
+              names["router.1"]]
+    log(f"[parity] full 6.78B, gradient norm and decay: 432 tensors, 4 steps, sampled {sample}")
+    st = run(wl, steps=4, sample=sample, hp=BOTH)
+    assert st.ok(), st
+
+
+def test_new_hparam_errors_launch_nothing():
+    dev = torch.device("cuda")
+    w = torch.ones((4, 8), dtype=torch.bfloat16, device=dev)
+    g = torch.ones_like(w)
+    opt = SkewAdam([(W.EXPERT, w, g, 0)])
+    from paper_2607_19058_amd import SkewError
+    for bad in (dict(weight_decay=-0.1), dict(weight_decay=float("nan")), dict(weight_decay=float("inf")),
+                dict(max_grad_norm=-1.0), dict(max_grad_norm=float("nan")), dict(max_grad_norm=float("inf"))):
+        with pytest.raises(SkewError):
+            opt.step(1, **bad)
+    torch.cuda.synchronize()
+    assert torch.equal(w, torch.ones_like(w))

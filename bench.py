@@ -107,6 +107,11 @@ def main() -> int:
     ap.add_argument("--workload", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--weight-decay", type=float, default=0.0,
+                    help="decoupled weight decay lambda fused into the update (router exempt)")
+    ap.add_argument("--max-grad-norm", type=float, default=0.0,
+                    help="> 0: the step scales the gradients by the global-norm factor (two-pass "
+                         "statistics); the bench also times torch's unfused clip_grad_norm_ on the same G")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three plain 1 GiB device-to-device copies (read 1 GiB, write 1 GiB "
                          "each), whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures")
@@ -146,7 +151,8 @@ def main() -> int:
         for k, s in enumerate(wl.specs):
             W.fill_grad(s, wl, t, G[k], sc)
 
-    hp = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0, seed=0)
+    hp = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0, seed=0,
+              weight_decay=args.weight_decay, max_grad_norm=args.max_grad_norm)
     for t in range(1, args.warmup + 1):
         draw(t)
         opt.step(t, **hp)
@@ -168,6 +174,28 @@ def main() -> int:
     per_kernel = opt.timing_read()
     steps_rec = per_kernel.pop("_steps")
     ev_ms = e0.elapsed_time(e1)
+    unfused_ms = None
+    if args.max_grad_norm > 0:
+        # what the fused scaling replaces: torch's clip_grad_norm_ on the same bf16 gradients
+        # (a norm read of G, then an in-place scale), timed on copies so G stays unchanged
+        Gc = [g.clone() for g in G]
+
+        def torch_clip():   # torch.nn.utils.clip_grad_norm_'s foreach path, on the tensors themselves
+            norms = torch._foreach_norm(Gc, 2.0)
+            total = torch.linalg.vector_norm(torch.stack([n_.float() for n_ in norms]), 2.0)
+            coef = torch.clamp(args.max_grad_norm / (total + 1e-6), max=1.0)
+            torch._foreach_mul_(Gc, coef.to(Gc[0].dtype))
+
+        torch_clip()
+        torch.cuda.synchronize()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        for _ in range(3):
+            torch_clip()
+        c1.record(stream)
+        torch.cuda.synchronize()
+        unfused_ms = c0.elapsed_time(c1) / 3
+        del Gc
 
     ms_per_step = 1e3 * wall / args.steps
     params = wl.numel
@@ -203,12 +231,14 @@ def main() -> int:
         "config": {"workload": f"{wl.name}: {params:,}-parameter synthetic MoE parameter set, {len(wl.specs)} tensors "
                                "(bf16 weights and gradients, fp32 state)",
                    "params": params, "tensors": len(wl.specs), "state_bytes": opt.state_nbytes,
-                   "workspace_bytes": opt.workspace_nbytes},
+                   "workspace_bytes": opt.workspace_nbytes, "weight_decay": args.weight_decay,
+                   "max_grad_norm": args.max_grad_norm},
         "roofline": roof,
         "step": {"algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3),
                  "effective_GBps": round(step_gbps, 1), "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),
                  "event_ms_per_step": round(ev_ms / args.steps, 4),
                  "kernel_ms_per_step": {k: round(v, 4) for k, v in kern_avg.items()}},
+        **({"torch_clip_grad_norm_ms": round(unfused_ms, 4)} if unfused_ms is not None else {}),
     }
     if not args.no_cpu_baseline:
         del Wt, G, opt

@@ -35,6 +35,7 @@ struct skew_ctx {
   RecheckLists *lists = nullptr;
   GroupedList p1, fold, p2, p3, clip, fold_rows;
   float *gscale = nullptr;   // device: the gradient-norm mode's scale
+  double *gsq = nullptr;     // device: per-tensor sums of g^2
   GroupedList z[kZVariants];   // row-band pass items, one list per kernel variant
   hipStream_t side = nullptr;  // the update pass of the pipeline runs here
   std::vector<hipEvent_t> sync;   // [0]: step start, [1]: update pass done, [2 + g]: group g ready
@@ -220,6 +221,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   add(c->fold_rows, p.fold_rows);
   if (items.empty()) items.push_back({0, 0});
   c->gscale = reinterpret_cast<float *>(ws + p.off_gscale);
+  c->gsq = reinterpret_cast<double *>(ws + p.off_gsq);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
@@ -250,6 +252,7 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
   StepConsts k = make_consts(*hp);
   k.gscale = ctx->gscale;
+  k.gsq = ctx->gsq;
   const Plan &p = ctx->plan;
   if (k.gclip && p.ngroups != 1) return SKEW_EINVAL;   // the global norm couples every tensor
   hipStream_t s0 = static_cast<hipStream_t>(stream), s1 = ctx->side;

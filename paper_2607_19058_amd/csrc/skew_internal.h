@@ -142,6 +142,7 @@ struct StepConsts {
   int32_t gclip;            // max_grad_norm > 0
   int32_t pad;
   float *gscale;            // device: the factor c (written by the norm stage)
+  double *gsq;              // device [ntensors]: each tensor's sum of g^2 (norm stage)
 };
 
 // Host-side plan of a descriptor table.
@@ -174,6 +175,7 @@ struct Plan {
   size_t off_lists = 0;                       // workspace offset of the RecheckLists
   size_t off_zero = 0;                        // workspace offset of 256 zero bytes
   size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)
+  size_t off_gsq = 0;                         // workspace offset of the per-tensor sums of g^2
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
   // fold items of the gradient-norm mode's first fold: rows and columns of every factored
   // tensor (row-band tensors: rows [0, ceil(n / kFold)), then columns)

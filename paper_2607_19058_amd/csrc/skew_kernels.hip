@@ -1033,24 +1033,26 @@ __global__ __launch_bounds__(kThreads) void gsq_kernel(const DevTensor *__restri
   if (threadIdx.x == 0) stg(t.ssum + it.tile, s);
 }
 
-// Gradient-norm mode: ||G||^2 over every tensor of the table in table order, then the scale
-// c = min(1, max_grad_norm / (||G|| + 1e-6)) (NaN propagates). One work-group.
-__global__ __launch_bounds__(kThreads) void gnorm_kernel(const DevTensor *__restrict__ TT, int ntensors,
-                                                         StepConsts k) {
+// Gradient-norm mode: ||G||^2 of each tensor (one work-group per tensor), then over the
+// table in table order and the scale c = min(1, max_grad_norm / (||G|| + 1e-6)) (NaN
+// propagates; one work-group)
+__global__ __launch_bounds__(kThreads) void gsum_kernel(const DevTensor *__restrict__ TT, StepConsts k) {
   __shared__ double sh[kThreads];
-  double total = 0.0;
-  for (int i = 0; i < ntensors; i++) {
-    const DevTensor &t = TT[i];
-    if (t.n * t.m == 0) continue;
-    double s;
+  const DevTensor &t = TT[blockIdx.x];
+  double s = 0.0;
+  if (t.n * t.m > 0) {
     if (t.kind != kFactored)
       s = wg_sum(t.ssum, (int64_t)t.ntr * t.ntc * kSub, sh);
     else if (t.zpath)
       s = wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double));
     else
       s = wg_sum(t.rowpart, (int64_t)t.ntc * t.n, sh);
-    total += s;
   }
+  if (threadIdx.x == 0) stg(k.gsq + blockIdx.x, s);
+}
+__global__ __launch_bounds__(kThreads) void gnorm_kernel(int ntensors, StepConsts k) {
+  __shared__ double sh[kThreads];
+  const double total = wg_sum(k.gsq, ntensors, sh);
   if (threadIdx.x == 0) {
     double c = (double)k.max_grad_norm / (sqrt(total) + 1e-6);
     if (c > 1.0) c = 1.0;
@@ -1702,7 +1704,11 @@ int launch_gsq(const DevTensor *T, const Item *items, int64_t count, void *strea
   return (int)hipGetLastError();
 }
 int launch_gnorm(const DevTensor *T, int ntensors, const StepConsts &k, void *stream) {
-  hipLaunchKernelGGL(gnorm_kernel, dim3(1), dim3(kThreads), 0, (hipStream_t)stream, T, ntensors, k);
+  if (ntensors <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gsum_kernel, dim3((uint32_t)ntensors), dim3(kThreads), 0, (hipStream_t)stream, T, k);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  hipLaunchKernelGGL(gnorm_kernel, dim3(1), dim3(kThreads), 0, (hipStream_t)stream, ntensors, k);
   return (int)hipGetLastError();
 }
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {

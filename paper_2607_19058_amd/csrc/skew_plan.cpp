@@ -163,6 +163,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   ws = align_up(ws + 256);
   p.off_gscale = ws;
   ws = align_up(ws + sizeof(float));
+  p.off_gsq = ws;
+  ws = align_up(ws + sizeof(double) * (size_t)std::max(n, 1));
   auto shift = [ws](size_t &off) {
     if (off != SIZE_MAX) off += ws;
   };

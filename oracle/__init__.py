@@ -25,6 +25,8 @@ TIER_NAMES = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
 # Paper defaults (Alg. 1 caption, Table 5): beta = (0.9, 0.999), eps = 1e-8,
 # lr = 3e-4; update clipping at RMS 1 (Sec. 3).
 DEFAULTS = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0)
+# tier variants of the ablation (Table 3): momentum in any tier; router matrices factored
+STATE_MOMENTUM, STATE_FACTORED = 1, 2
 
 
 def build(verbose: bool = False) -> str:
@@ -48,6 +50,7 @@ class _Tensor(ctypes.Structure):
         ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
         ("u_out", ctypes.c_void_p), ("x_out", ctypes.c_void_p), ("y_out", ctypes.c_void_p),
         ("rms_out", ctypes.c_void_p),
+        ("batch", ctypes.c_int64), ("state_flags", ctypes.c_uint32),
     ]
 
 
@@ -110,29 +113,43 @@ class Tensor:
     x_out: Optional[np.ndarray] = field(default=None, repr=False)
     y_out: Optional[np.ndarray] = field(default=None, repr=False)
     rms: float = float("nan")
+    state_flags: int = 0          # STATE_MOMENTUM | STATE_FACTORED (tier variants, Table 3)
 
     @property
     def ndim(self) -> int:
         return self.w.ndim
 
     @property
+    def batch(self) -> int:
+        """E for a stacked (E, rows, cols) tensor, else 1."""
+        return int(self.w.shape[0]) if self.w.ndim == 3 else 1
+
+    @property
     def rows_cols(self):
         if self.w.ndim == 1:
             return 1, int(self.w.shape[0])
-        return int(self.w.shape[0]), int(self.w.shape[1])
+        return int(self.w.shape[-2]), int(self.w.shape[-1])
+
+    @property
+    def exact(self) -> bool:
+        return (self.tier == ROUTER and not (self.state_flags & STATE_FACTORED)) or self.ndim == 1
+
+    @property
+    def momentum(self) -> bool:
+        return self.tier == BACKBONE or bool(self.state_flags & STATE_MOMENTUM)
 
     def init_state(self):
-        """Allocate zeroed state for this tensor's tier (Fig. 1, Table 6)."""
+        """Allocate zeroed state for this tensor's tier (Fig. 1, Table 6) and variant
+        (Table 3); a stacked tensor keeps R [E, rows] and C [E, cols]."""
         n, m = self.rows_cols
         shape = self.w.shape
-        exact = self.tier == ROUTER or self.ndim == 1
-        if self.tier == BACKBONE:
+        if self.momentum:
             self.m = np.zeros(shape, np.float32)
-        if exact:
+        if self.exact:
             self.v = np.zeros(shape, np.float32)
         else:
-            self.r = np.zeros(n, np.float32)
-            self.c = np.zeros(m, np.float32)
+            self.r = np.zeros((self.batch, n) if self.ndim == 3 else n, np.float32)
+            self.c = np.zeros((self.batch, m) if self.ndim == 3 else m, np.float32)
         return self
 
 
@@ -158,14 +175,14 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
                 assert a.flags["C_CONTIGUOUS"], name
         assert t.w.dtype == np.uint16 and t.g.dtype == np.uint16 and t.w.shape == t.g.shape
         n, m = t.rows_cols
-        exact = t.tier == ROUTER or t.ndim == 1
+        E = t.batch
         if n * m > 0:
-            if t.tier == BACKBONE:
-                assert t.m is not None and t.m.dtype == np.float32 and t.m.size == n * m
-            if exact:
-                assert t.v is not None and t.v.dtype == np.float32 and t.v.size == n * m
+            if t.momentum:
+                assert t.m is not None and t.m.dtype == np.float32 and t.m.size == E * n * m
+            if t.exact:
+                assert t.v is not None and t.v.dtype == np.float32 and t.v.size == E * n * m
             else:
-                assert t.r is not None and t.r.size == n and t.c is not None and t.c.size == m
+                assert t.r is not None and t.r.size == E * n and t.c is not None and t.c.size == E * m
         if want_u:
             t.u_out = np.empty(t.w.shape, np.float32)
         if want_x:
@@ -174,7 +191,7 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
             t.y_out = np.empty(t.w.shape, np.float32)
         arr[k] = _Tensor(t.tier, t.ndim, n, m, t.tensor_id, _ptr(t.w), _ptr(t.g), _ptr(t.m), _ptr(t.v),
                          _ptr(t.r), _ptr(t.c), _ptr(t.u_out), _ptr(t.x_out), _ptr(t.y_out),
-                         rms.ctypes.data + 8 * k)
+                         rms.ctypes.data + 8 * k, E if t.ndim == 3 else 0, int(t.state_flags))
         keep.append(t)
     hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1),
                   weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total))

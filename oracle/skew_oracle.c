@@ -30,6 +30,10 @@
  *       y = fmaf(e*2^-24, |w|, x);  W' = bf16 round-to-nearest-even(y)
  *   max() here propagates NaN (as torch.clamp does), so non-finite gradients
  *   reach the weights instead of being floored away.
+ * Tier variants (Table 3) switch momentum on in any tier (then s_m applies) and the
+ * factored second moment on for router matrices. A stacked tensor of E matrices
+ * (ndim 3) is factored per slice, each slice with its own R, C and mean(R); the clip,
+ * the dither's element index and N run over the whole tensor.
  */
 #include "skew_oracle.h"
 #include <math.h>
@@ -122,51 +126,62 @@ int skew_oracle_threads(void) {
 
 static float max_nan(float a, float b) { return (a != a) ? a : (a < b ? b : a); }
 
+/* Eq. 1 and the rank-one reconstruction for one n x m matrix (one slice of a stacked
+ * tensor): updates R [n] and C [m] in place and writes c'_j = C_j / max(mean R, eps). */
+static void factored_stats(const consts_t *K, const uint16_t *g, float *R, float *C, int64_t n, int64_t m,
+                           float *cprime) {
+  /* rows: mean over columns of G*G, then the EMA of R */
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; i++) {
+    double s = 0.0;
+    for (int64_t j = 0; j < m; j++) {
+      double gv = bf16_bits_to_f32(g[i * m + j]);
+      s += gv * gv;
+    }
+    /* with gradient-norm scaling the statistic is c^2 times the exact sum */
+    float ri = (float)((K->gclip ? K->gc2 * s : s) / (double)m);
+    R[i] = fmaf(K->a2, ri, K->b2 * R[i]);
+  }
+  /* columns: mean over rows of G*G (each column summed in row order) */
+  double *cs = (double *)calloc((size_t)m, sizeof(double));
+#pragma omp parallel for schedule(static)
+  for (int64_t jb = 0; jb < m; jb += COL_BLOCK) {
+    int64_t je = jb + COL_BLOCK < m ? jb + COL_BLOCK : m;
+    for (int64_t i = 0; i < n; i++)
+      for (int64_t j = jb; j < je; j++) {
+        double gv = bf16_bits_to_f32(g[i * m + j]);
+        cs[j] += gv * gv;
+      }
+  }
+  for (int64_t j = 0; j < m; j++) {
+    float cj = (float)((K->gclip ? K->gc2 * cs[j] : cs[j]) / (double)n);
+    C[j] = fmaf(K->a2, cj, K->b2 * C[j]);
+  }
+  free(cs);
+  /* rank-one reconstruction V = R C^T / mean(R), with the mean clamped at eps */
+  double sr = 0.0;
+  for (int64_t i = 0; i < n; i++) sr += (double)R[i];
+  float rbar = (float)(sr / (double)n);
+  float q = max_nan(rbar, K->eps);
+  for (int64_t j = 0; j < m; j++) cprime[j] = C[j] / q;
+}
+
 static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
-  const int64_t n = T->rows, m = T->cols, N = n * m;
-  if (n <= 0 || m <= 0) return;
-  const int exact = (T->tier == ORACLE_ROUTER) || (T->ndim == 1);
-  const int momentum = (T->tier == ORACLE_BACKBONE);
+  /* a stacked tensor is E slices of rows x cols; row ii of the stacked rows is row
+     ii % rows of slice ii / rows, and r holds the slices' R one after the other */
+  const int64_t E = (T->ndim == 3 && T->batch > 0) ? T->batch : 1;
+  const int64_t n1 = T->rows, m = T->cols, n = E * n1, N = n * m;
+  if (n1 <= 0 || m <= 0) return;
+  const int exact = (T->tier == ORACLE_ROUTER && !(T->state_flags & ORACLE_STATE_FACTORED)) || (T->ndim == 1);
+  const int momentum = (T->tier == ORACLE_BACKBONE) || (T->state_flags & ORACLE_STATE_MOMENTUM);
   float *uhat = (float *)malloc((size_t)N * sizeof(float));
   double *row_ss = (double *)malloc((size_t)n * sizeof(double));
   float *cprime = NULL;
 
   if (!exact) {
-    /* Eq. 1, rows: mean over columns of G*G, then the EMA of R. */
-#pragma omp parallel for schedule(static)
-    for (int64_t i = 0; i < n; i++) {
-      double s = 0.0;
-      for (int64_t j = 0; j < m; j++) {
-        double gv = bf16_bits_to_f32(T->g[i * m + j]);
-        s += gv * gv;
-      }
-      /* with gradient-norm scaling the statistic is c^2 times the exact sum */
-      float ri = (float)((K->gclip ? K->gc2 * s : s) / (double)m);
-      T->r[i] = fmaf(K->a2, ri, K->b2 * T->r[i]);
-    }
-    /* Eq. 1, columns: mean over rows of G*G (each column summed in row order). */
-    double *cs = (double *)calloc((size_t)m, sizeof(double));
-#pragma omp parallel for schedule(static)
-    for (int64_t jb = 0; jb < m; jb += COL_BLOCK) {
-      int64_t je = jb + COL_BLOCK < m ? jb + COL_BLOCK : m;
-      for (int64_t i = 0; i < n; i++)
-        for (int64_t j = jb; j < je; j++) {
-          double gv = bf16_bits_to_f32(T->g[i * m + j]);
-          cs[j] += gv * gv;
-        }
-    }
-    for (int64_t j = 0; j < m; j++) {
-      float cj = (float)((K->gclip ? K->gc2 * cs[j] : cs[j]) / (double)n);
-      T->c[j] = fmaf(K->a2, cj, K->b2 * T->c[j]);
-    }
-    free(cs);
-    /* rank-one reconstruction V = R C^T / mean(R), with the mean clamped at eps */
-    double sr = 0.0;
-    for (int64_t i = 0; i < n; i++) sr += (double)T->r[i];
-    float rbar = (float)(sr / (double)n);
-    float q = max_nan(rbar, K->eps);
-    cprime = (float *)malloc((size_t)m * sizeof(float));
-    for (int64_t j = 0; j < m; j++) cprime[j] = T->c[j] / q;
+    cprime = (float *)malloc((size_t)(E * m) * sizeof(float));
+    for (int64_t e = 0; e < E; e++)
+      factored_stats(K, T->g + e * n1 * m, T->r + e * n1, T->c + e * m, n1, m, cprime + e * m);
   }
 
   /* preconditioned update and its sum of squares, row by row */
@@ -182,7 +197,7 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
         T->v[idx] = fmaf(K->a2, g * g, K->b2 * T->v[idx]);
         dd = sqrtf(max_nan(T->v[idx], K->eps));
       } else {
-        float vhat = T->r[i] * cprime[j];
+        float vhat = T->r[i] * cprime[(i / n1) * m + j];
         dd = sqrtf(max_nan(vhat, K->eps));
       }
       float num;
@@ -257,7 +272,8 @@ int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t,
     /* global 2-norm over every element of every tensor, in double, in order */
     double total = 0.0;
     for (int i = 0; i < n && hp->gsq_total < 0.0; i++) {
-      const int64_t N = t[i].rows * t[i].cols;
+      const int64_t E = (t[i].ndim == 3 && t[i].batch > 0) ? t[i].batch : 1;
+      const int64_t N = E * t[i].rows * t[i].cols;
       for (int64_t idx = 0; idx < N; idx++) {
         const double gv = bf16_bits_to_f32(t[i].g[idx]);
         total += gv * gv;

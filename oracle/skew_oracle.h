@@ -35,7 +35,14 @@ typedef struct {
   float *x_out;       /* optional [rows*cols]: W - lr*U before the dither */
   float *y_out;       /* optional [rows*cols]: the float value handed to the bf16 cast */
   double *rms_out;    /* optional: RMS of the unclipped update of this tensor */
+  int64_t batch;      /* ndim 3: E >= 1 stacked rows x cols matrices (w, g, m, v [E][rows][cols],
+                         r [E][rows], c [E][cols]), factored per slice, one clip over all;
+                         0 or 1 otherwise */
+  uint32_t state_flags; /* ORACLE_STATE_*: tier variants of the ablation (Table 3) */
 } skew_oracle_tensor;
+
+/* Tier variants (Table 3): momentum kept in any tier; router matrices factored. */
+enum { ORACLE_STATE_MOMENTUM = 1, ORACLE_STATE_FACTORED = 2 };
 
 typedef struct {
   float lr, beta1, beta2, eps, clip_threshold;

@@ -25,9 +25,9 @@ def f32(b) -> np.ndarray:
     return oracle.bf16_to_f32(b)
 
 
-def make(tier, w, tid=0):
+def make(tier, w, tid=0, flags=0):
     w = np.ascontiguousarray(w, np.uint16)
-    return oracle.Tensor(tier=tier, w=w.copy(), g=np.zeros_like(w), tensor_id=tid).init_state()
+    return oracle.Tensor(tier=tier, w=w.copy(), g=np.zeros_like(w), tensor_id=tid, state_flags=flags).init_state()
 
 
 def rank1_grads(rng, n, m, steps):
@@ -227,3 +227,91 @@ def test_gradnorm_nonfinite_norm_propagates():
     # inf norm: the scale is 0 and inf * 0 is NaN
     assert oracle.last_gcoef() == 0.0
     assert np.isnan(f32(T.w)).any()
+
+
+# ----------------------------------------------------------------------------- tier variants
+def _variant_adam(tier, flags, shape, grads, beta1):
+    rng = np.random.default_rng(31)
+    T = make(tier, bf16(rng.normal(0, 0.02, shape)), 7, flags)
+    p = torch.zeros(shape, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([p], lr=LR, betas=(beta1, B2), eps=0.0, foreach=False)
+    for t, g in enumerate(grads, start=1):
+        T.g = g
+        w_before = f32(T.w).astype(np.float64)
+        with torch.no_grad():
+            p.copy_(torch.from_numpy(w_before))
+        p.grad = torch.from_numpy(f32(g).astype(np.float64))
+        opt.step()
+        oracle.step([T], t, eps=1e-30, clip_threshold=float("inf"), want_u=True, want_x=True)
+        np.testing.assert_allclose(T.u_out, (w_before - p.detach().numpy()) / LR, rtol=3e-6, atol=3e-6)
+        np.testing.assert_allclose(T.x_out, p.detach().numpy(), rtol=1e-7, atol=2e-9)
+    return T
+
+
+def test_variant_expert_momentum_is_adam():
+    """Table 3 '+ momentum on experts': a rank-one expert matrix with momentum is Adam."""
+    rng = np.random.default_rng(32)
+    T = _variant_adam(E, oracle.STATE_MOMENTUM, (6, 11), rank1_grads(rng, 6, 11, 6), beta1=B1)
+    assert T.m is not None and T.r is not None and T.v is None
+
+
+def test_variant_factored_router_is_adam_without_momentum():
+    """Table 3 'factored router': a rank-one router matrix, factored, is Adam(beta1 = 0)."""
+    rng = np.random.default_rng(33)
+    T = _variant_adam(R, oracle.STATE_FACTORED, (9, 8), rank1_grads(rng, 9, 8, 6), beta1=0.0)
+    assert T.v is None and T.r is not None and T.m is None
+
+
+def test_variant_uniform_router_is_adam():
+    """Table 3 'uniform (momentum + factored)': the router with both is Adam(beta1, beta2)."""
+    rng = np.random.default_rng(34)
+    _variant_adam(R, oracle.STATE_MOMENTUM | oracle.STATE_FACTORED, (7, 12), rank1_grads(rng, 7, 12, 6),
+                  beta1=B1)
+
+
+def test_variant_router_vector_stays_exact():
+    T = make(R, bf16(np.full(16, 0.01)), 0, oracle.STATE_FACTORED)
+    assert T.v is not None and T.r is None      # vectors keep the exact second moment (Alg. 1)
+
+
+# ----------------------------------------------------------------------------- stacked tensors
+@pytest.mark.parametrize("tier", [E, B])
+def test_stacked_equals_separate_slices(tier):
+    """A stacked (E, n, m) tensor factors per slice (Sec. 3 footnote): without the clip
+    binding, each slice's R, C, M, update and pre-dither weight equal those of the slice
+    stepped alone; the clip's RMS runs over the whole tensor."""
+    rng = np.random.default_rng(41)
+    Eb, n, m = 4, 6, 10
+    w0 = bf16(rng.normal(0, 0.02, (Eb, n, m)))
+    S = make(tier, w0, 9)
+    parts = [make(tier, w0[e], 100 + e) for e in range(Eb)]
+    for t in range(1, 4):
+        scale = 10.0 ** rng.uniform(-4, -1, Eb)
+        g = bf16(rng.normal(0, 1, (Eb, n, m)) * scale[:, None, None])
+        S.g = g
+        oracle.step([S], t, clip_threshold=float("inf"), want_u=True, want_x=True)
+        ss = 0.0
+        for e, P in enumerate(parts):
+            P.g = g[e].copy()
+            oracle.step([P], t, clip_threshold=float("inf"), want_u=True, want_x=True)
+            assert np.array_equal(S.r[e], P.r) and np.array_equal(S.c[e], P.c)
+            if tier == B:
+                assert np.array_equal(S.m[e], P.m)
+            assert np.array_equal(S.u_out[e], P.u_out)
+            ss += P.rms ** 2 * n * m
+        assert abs(S.rms ** 2 * Eb * n * m - ss) <= 1e-12 * ss
+        # keep the slices' weights equal to the stacked ones (the dither differs by index)
+        for e, P in enumerate(parts):
+            P.w = S.w[e].copy()
+
+
+def test_stacked_clip_runs_over_the_whole_tensor():
+    rng = np.random.default_rng(42)
+    Eb, n, m = 3, 5, 8
+    S = make(E, bf16(rng.normal(0, 0.02, (Eb, n, m))), 1)
+    g = rng.normal(0, 1e-3, (Eb, n, m))
+    g[1] *= 30.0                       # one slice dominates the update's RMS
+    S.g = bf16(g)
+    oracle.step([S], 1, clip_threshold=0.5, want_u=True)
+    rms_after = float(np.sqrt(np.mean(S.u_out.astype(np.float64) ** 2)))
+    assert S.rms > 0.5 and abs(rms_after - 0.5) <= 1e-6     # one factor k for all slices

@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define SKEW_ABI_VERSION 2
+#define SKEW_ABI_VERSION 3
 
 enum {
   SKEW_OK = 0,
@@ -49,10 +49,21 @@ enum { SKEW_TIER_BACKBONE = 0, SKEW_TIER_EXPERT = 1, SKEW_TIER_ROUTER = 2 };
 
 enum { SKEW_FLAG_EXACT_CLIP = 1 };
 
+/* Per-tensor state variants (the tier ablation, Table 3): SKEW_STATE_MOMENTUM keeps fp32
+ * momentum in any tier (then the bias correction of the backbone applies);
+ * SKEW_STATE_FACTORED gives router matrices the factored second moment. Vectors always
+ * keep the exact one (Alg. 1). "+ momentum on experts" is MOMENTUM on the expert tensors,
+ * "factored router" FACTORED on the router, "uniform" both on every tensor. */
+enum { SKEW_STATE_MOMENTUM = 1, SKEW_STATE_FACTORED = 2 };
+
 /* One parameter tensor (Sec. 3 "The tiers": the policy assigns state by parameter role).
  *   tier      SKEW_TIER_*.
  *   ndim      2 = matrix (row-major, `rows` x `cols`, row stride `ld` elements);
- *             1 = vector of rows*cols elements (one of rows, cols must be 1), contiguous.
+ *             1 = vector of rows*cols elements (one of rows, cols must be 1), contiguous;
+ *             3 = `batch` stacked matrices of `rows` x `cols` (slice stride rows*ld
+ *             elements), factored along the last two axes, each slice with its own R, C
+ *             and mean(R) (Sec. 3 footnote); the clip factor, N and the dither's element
+ *             index (e*rows*cols + i*cols + j) run over the whole tensor.
  *             Matrices outside the router tier take the factored second moment (Eq. 1);
  *             the router and every vector take the exact one (Alg. 1).
  *   rows, cols  >= 0. A tensor with no elements is accepted and skipped.
@@ -63,7 +74,10 @@ enum { SKEW_FLAG_EXACT_CLIP = 1 };
  *   g         device, bf16 [rows x ld], read only.
  *   m, v, r, c  OUT: filled by skew_state_init with pointers into the caller's state
  *             buffer (NULL where the tier keeps no such state); dense, row-major:
- *             m, v [rows*cols] (element (i, j) at i*cols + j), r [rows], c [cols].
+ *             m, v [rows*cols] (element (i, j) at i*cols + j), r [rows], c [cols];
+ *             stacked: m, v [batch][rows][cols], r [batch][rows], c [batch][cols].
+ *   batch     ndim 3: the number of slices (>= 0; 0 = no elements); otherwise 0 or 1.
+ *   state_flags  0 or SKEW_STATE_* bits (tier variants, Table 3).
  * w and g may have any alignment; 16-byte-aligned rows (w, g aligned and ld a
  * multiple of 8) take the vectorised path. */
 typedef struct skew_tensor_desc {
@@ -79,6 +93,9 @@ typedef struct skew_tensor_desc {
   float *v;
   float *r;
   float *c;
+  int64_t batch;
+  uint32_t state_flags;
+  uint32_t reserved;
 } skew_tensor_desc;
 
 /* Hyper-parameters of one step (Alg. 1; defaults of Table 5: lr 3e-4,

@@ -132,28 +132,37 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   if (rc != SKEW_OK) return rc;
   if (state_bytes < p.state_bytes || workspace_bytes < p.ws_bytes) return SKEW_ENOSPACE;
   if ((p.state_bytes > 0 && state == nullptr) || workspace == nullptr) return SKEW_EINVAL;
-  for (int i = 0; i < n; i++)
-    if (!p.t[i].empty && (d[i].w == nullptr || d[i].g == nullptr)) return SKEW_EINVAL;
+  const int nt = (int)p.t.size();   // sub-tensors (a stacked tensor's slices are several)
+  for (int i = 0; i < nt; i++)
+    if (!p.t[i].empty && (d[p.t[i].desc].w == nullptr || d[p.t[i].desc].g == nullptr)) return SKEW_EINVAL;
 
   char *st = static_cast<char *>(state);
   char *ws = static_cast<char *>(workspace);
   auto sp = [&](size_t off) { return off == SIZE_MAX ? nullptr : reinterpret_cast<float *>(st + off); };
-  std::vector<DevTensor> table((size_t)(n > 0 ? n : 1));
+  for (int di = 0; di < n; di++) {   // the caller's view: each descriptor's state from its first slice
+    const TensorPlan &tp = p.t[(size_t)p.desc_sub0[(size_t)di]];
+    d[di].m = sp(tp.off_m);
+    d[di].v = sp(tp.off_v);
+    d[di].r = sp(tp.off_r);
+    d[di].c = sp(tp.off_c);
+  }
+  std::vector<DevTensor> table((size_t)(nt > 0 ? nt : 1));
   std::memset(table.data(), 0, sizeof(DevTensor) * table.size());
-  for (int i = 0; i < n; i++) {
+  for (int i = 0; i < nt; i++) {
     const TensorPlan &tp = p.t[i];
-    d[i].m = sp(tp.off_m);
-    d[i].v = sp(tp.off_v);
-    d[i].r = sp(tp.off_r);
-    d[i].c = sp(tp.off_c);
     if (tp.empty) continue;
+    const skew_tensor_desc &dd = d[tp.desc];
+    const int64_t slice = (int64_t)(i - tp.grp0) * tp.n * tp.ld;   // elements to this slice's first row
     DevTensor &x = table[i];
-    x.w = static_cast<uint16_t *>(d[i].w);
-    x.g = static_cast<const uint16_t *>(d[i].g);
-    x.M = d[i].m;
-    x.V = d[i].v;
-    x.R = d[i].r;
-    x.C = d[i].c;
+    x.w = static_cast<uint16_t *>(dd.w) + slice;
+    x.g = static_cast<const uint16_t *>(dd.g) + slice;
+    x.M = sp(tp.off_m);
+    x.V = sp(tp.off_v);
+    x.R = sp(tp.off_r);
+    x.C = sp(tp.off_c);
+    x.idx0 = tp.idx0;
+    x.grp0 = tp.grp0;
+    x.ngrp = tp.ngrp;
     x.ssum = reinterpret_cast<double *>(ws + tp.off_ssum);
     x.qsum = reinterpret_cast<double *>(ws + tp.off_qsum);
     x.sc = reinterpret_cast<TensorScalars *>(ws + tp.off_sc);
@@ -185,8 +194,8 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.kind = tp.kind;
     x.decay = tp.tier != SKEW_TIER_ROUTER ? 1 : 0;
     x.momentum = tp.momentum;
-    x.vec = aligned16(d[i].w) && aligned16(d[i].g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
-    x.tensor_id = d[i].tensor_id;
+    x.vec = aligned16(x.w) && aligned16(x.g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
+    x.tensor_id = dd.tensor_id;
   }
   // row-band pass items by kernel variant (16-byte aligned rows or element loads is known
   // only here, from the pointers); every list keeps tensor order, so each pipeline group
@@ -387,12 +396,14 @@ const char *skew_launch_name(skew_ctx *ctx, int j) {
 }
 
 int skew_clip_info(skew_ctx *ctx, float *k, int32_t *route, int n, void *stream) {
-  if (ctx == nullptr || k == nullptr || route == nullptr || n < (int)ctx->plan.t.size()) return SKEW_EINVAL;
+  const int nd = ctx ? (int)ctx->plan.desc_sub0.size() : 0;
+  if (ctx == nullptr || k == nullptr || route == nullptr || n < nd) return SKEW_EINVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int nt = (int)ctx->plan.t.size();
+  // per descriptor: the scalars of its first sub-tensor (a stacked tensor's slices share k)
+  const int nt = nd;
   std::vector<TensorScalars> sc((size_t)std::max(nt, 1));
   for (int i = 0; i < nt; i++) {
-    const TensorPlan &tp = ctx->plan.t[i];
+    const TensorPlan &tp = ctx->plan.t[(size_t)ctx->plan.desc_sub0[(size_t)i]];
     if (tp.empty) {
       std::memset(&sc[i], 0, sizeof(TensorScalars));
       continue;
@@ -403,7 +414,8 @@ int skew_clip_info(skew_ctx *ctx, float *k, int32_t *route, int n, void *stream)
   if (hipStreamSynchronize(s) != hipSuccess) return SKEW_EHIP;
   for (int i = 0; i < nt; i++) {
     k[i] = sc[i].k;
-    route[i] = (sc[i].ambiguous & 0xFF) | ((ctx->plan.t[i].zpath ? sc[i].regime & 0xFF : 0) << 8);
+    const TensorPlan &tp = ctx->plan.t[(size_t)ctx->plan.desc_sub0[(size_t)i]];
+    route[i] = (sc[i].ambiguous & 0xFF) | ((tp.zpath ? sc[i].regime & 0xFF : 0) << 8);
   }
   return SKEW_OK;
 }

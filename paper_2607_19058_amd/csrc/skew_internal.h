@@ -122,7 +122,10 @@ struct DevTensor {
   int32_t nzb;            // row-band pass: row bands
   int32_t zrb;            // row-band pass: rows per group and block
   int32_t decay;          // the decoupled weight decay applies (every tier but the router)
-  int64_t zrows;          // row-band pass: rows per band
+  int64_t zrows;
+  int64_t idx0;           // element index of this (sub-)tensor's first element in the caller's
+                          // tensor: a stacked tensor's slices are sub-tensors (dither index)
+  int32_t grp0, ngrp;     // the sub-tensors that share one clip factor: [grp0, grp0 + ngrp)          // row-band pass: rows per band
   uint64_t tensor_id;
 };
 
@@ -147,6 +150,9 @@ struct StepConsts {
 
 // Host-side plan of a descriptor table.
 struct TensorPlan {
+  int32_t desc = 0;            // descriptor this sub-tensor comes from
+  int32_t grp0 = 0, ngrp = 1;  // the sub-tensors sharing its clip factor (a stacked tensor's slices)
+  int64_t idx0 = 0;            // element index of its first element in the descriptor's tensor
   int64_t n = 0, m = 0, ld = 0, N = 0;
   int32_t tier = 0, kind = 0, momentum = 0;
   int64_t tr = 0;
@@ -171,7 +177,8 @@ struct TensorPlan {
 constexpr int kMaxGroups = 1;
 
 struct Plan {
-  std::vector<TensorPlan> t;
+  std::vector<TensorPlan> t;                  // sub-tensors (the device table's entries)
+  std::vector<int32_t> desc_sub0, desc_nsub;  // per descriptor: its first sub-tensor and their count
   size_t off_lists = 0;                       // workspace offset of the RecheckLists
   size_t off_zero = 0;                        // workspace offset of 256 zero bytes
   size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)

@@ -1332,23 +1332,35 @@ __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor 
   const int n = ldg(level == 1 ? &L->n1 : &L->n2);
   if ((int)blockIdx.x >= n) return;
   const int ti = ldg(recheck_list(L, ntensors, level) + blockIdx.x);
-  const DevTensor &t = TT[ti];
-  const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
-  const double S = wg_sum(t.ssum, ntiles, sh);
-  const double Q4 = level == 1 ? wg_sum(t.qsum, ntiles, sh) : 0.0;
+  const DevTensor &t0 = TT[ti];
+  // a group's slices are listed together; its first slice decides k for all of them
+  if (t0.grp0 != ti) return;
+  const int ng = t0.ngrp;
+  double S = 0.0, Q4 = 0.0, N = 0.0;
+  for (int e = 0; e < ng; e++) {
+    const DevTensor &t = TT[ti + e];
+    const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
+    S += wg_sum(t.ssum, ntiles, sh);
+    if (level == 1) Q4 += wg_sum(t.qsum, ntiles, sh);
+    N += (double)(t.n * t.m);
+  }
   if (threadIdx.x != 0) return;
   bool amb = false;
   const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
-  const float kf = clip_from_sum(S, (double)(t.n * t.m), k.d, spread, amb);
-  const int why = ldg(&t.sc->ambiguous) & ~0xF;
+  const float kf = clip_from_sum(S, N, k.d, spread, amb);
+  const int why = ldg(&t0.sc->ambiguous) & ~0xF;
   if (amb) {
-    const int pos = atomicAdd(&L->n2, 1);
-    stg(recheck_list(L, ntensors, 2) + pos, (int32_t)ti);
-    stg(&t.sc->ambiguous, (int32_t)(kClipPending2 | (kWhySpread << 4)));
+    const int pos = atomicAdd(&L->n2, ng);
+    for (int e = 0; e < ng; e++) {
+      stg(recheck_list(L, ntensors, 2) + pos + e, (int32_t)(ti + e));
+      stg(&TT[ti + e].sc->ambiguous, (int32_t)(kClipPending2 | (kWhySpread << 4)));
+    }
     return;
   }
-  stg(&t.sc->k, kf);
-  stg(&t.sc->ambiguous, (int32_t)(why | (level == 1 ? kClipSplit : kClipExact)));
+  for (int e = 0; e < ng; e++) {
+    stg(&TT[ti + e].sc->k, kf);
+    stg(&TT[ti + e].sc->ambiguous, (int32_t)(why | (level == 1 ? kClipSplit : kClipExact)));
+  }
 }
 
 // --------------------------------------------------------------------------------------------
@@ -1370,88 +1382,113 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
                                                         const Item *__restrict__ items, StepConsts k,
                                                         RecheckLists *L, int ntensors) {
   __shared__ double sh[kThreads];
-  const Item it = items[blockIdx.x];
-  const DevTensor &t = TT[it.tensor];
-  const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
-  const double N = (double)(t.n * t.m);
-  const float q = t.kind == kFactored ? mean_r_clamped(t, k, sh) : 0.f;
-  double S = 0.0, spread = 0.0;
-  bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t.kind == kFactored;
+  const Item it = items[blockIdx.x];   // the first sub-tensor of a group sharing one k
+  const DevTensor &t0 = TT[it.tensor];
+  const int g0 = t0.grp0, ng = t0.ngrp;
+  // the group's sum S as the sum of its slices' estimates, with the sum of their absolute
+  // error bounds; a slice whose floor regime leaves its sum open contributes an upper bound
+  double S = 0.0, err = 0.0, N = 0.0;
+  bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t0.kind == kFactored;
   int why = amb ? kWhyForced : 0;
-  int level = 2;   // the re-check a flagged tensor gets
-  if (t.zpath) {
-    const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
-    const double Y = wg_sum(&t.bst->ysum, t.nzb, sh, bstride);
-    const double SU = wg_sum(&t.cst->s, t.nfc, sh, cstride);
-    double um = 0.0;
-    float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
-    int bad = 0;
-    for (int64_t b = threadIdx.x; b < t.nzb; b += kThreads) {
-      um = fmax(um, ldg(&t.bst[b].umax));
-      rmn = fminf(rmn, ldg(&t.bst[b].rmin));
-      rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
-      bad |= ldg(&t.bst[b].bad);
-    }
-    for (int64_t c = threadIdx.x; c < t.nfc; c += kThreads) {
-      cmn = fminf(cmn, ldg(&t.cst[c].cmin));
-      cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
-      bad |= ldg(&t.cst[c].bad);
-    }
-    um = wg_max_w<kWaves>(um, sh);
-    rmn = wg_min_wf<kWaves>(rmn, sh);
-    rmx = wg_max_wf<kWaves>(rmx, sh);
-    cmn = wg_min_wf<kWaves>(cmn, sh);
-    cmx = wg_max_wf<kWaves>(cmx, sh);
-    bad = wg_or_w<kWaves>(bad, sh);
-    if (threadIdx.x != 0) return;
-    // the sums the row-band pass formed this step (it skips one when the last step predicts
-    // the regime); a sum it did not form counts as +inf
-    const int formed = ldg(&t.bst[0].regime);
-    const bool have_z = formed != kRegimeFloor, have_y = formed != kRegimeAbove;
-    const double inf = __builtin_inf();
-    const double SUf = have_z ? SU : inf, Yf = have_y ? Y : inf;
-    const bool finite = !(SUf != SUf) && !(Yf != Yf) && (SUf < 1e300 || Yf < 1e300);
-    const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
-    if (bad || !finite) {
-      amb = true;
-      why = kWhyNonFinite;
-      S = SU;
-    } else if (have_z && lo >= k.eps) {   // nothing on the floor
-      S = SU;
-      spread = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) / SU + 1e-14 : 0.0;
-    } else if (have_y && hi < k.eps) {    // everything on the floor
-      S = Y;
-      spread = 1e-14;
-    } else {
-      S = fmin(SUf, Yf) * (1.0 + 1e-6);   // an upper bound of the oracle's sum
-      if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
-        amb = true;
-        why = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
-        level = 1;   // the floor split per element decides most of these
+  bool open = false, bad_any = false;
+  for (int e = 0; e < ng; e++) {
+    const DevTensor &t = TT[g0 + e];
+    N += (double)(t.n * t.m);
+    const float q = t.kind == kFactored ? mean_r_clamped(t, k, sh) : 0.f;
+    double Se = 0.0, Ee = 0.0;   // the slice's estimate and its error bound
+    if (t.zpath) {
+      const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
+      const double Y = wg_sum(&t.bst->ysum, t.nzb, sh, bstride);
+      const double SU = wg_sum(&t.cst->s, t.nfc, sh, cstride);
+      double um = 0.0;
+      float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
+      int bad = 0;
+      for (int64_t b = threadIdx.x; b < t.nzb; b += kThreads) {
+        um = fmax(um, ldg(&t.bst[b].umax));
+        rmn = fminf(rmn, ldg(&t.bst[b].rmin));
+        rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
+        bad |= ldg(&t.bst[b].bad);
       }
+      for (int64_t c = threadIdx.x; c < t.nfc; c += kThreads) {
+        cmn = fminf(cmn, ldg(&t.cst[c].cmin));
+        cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
+        bad |= ldg(&t.cst[c].bad);
+      }
+      um = wg_max_w<kWaves>(um, sh);
+      rmn = wg_min_wf<kWaves>(rmn, sh);
+      rmx = wg_max_wf<kWaves>(rmx, sh);
+      cmn = wg_min_wf<kWaves>(cmn, sh);
+      cmx = wg_max_wf<kWaves>(cmx, sh);
+      bad = wg_or_w<kWaves>(bad, sh);
+      if (threadIdx.x == 0) {
+        // the sums the row-band pass formed this step (it skips one when the last step
+        // predicts the regime); a sum it did not form counts as +inf
+        const int formed = ldg(&t.bst[0].regime);
+        const bool have_z = formed != kRegimeFloor, have_y = formed != kRegimeAbove;
+        const double inf = __builtin_inf();
+        const double SUf = have_z ? SU : inf, Yf = have_y ? Y : inf;
+        const bool finite = !(SUf != SUf) && !(Yf != Yf) && (SUf < 1e300 || Yf < 1e300);
+        const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
+        if (bad || !finite) {
+          bad_any = true;
+          Se = SU;
+        } else if (have_z && lo >= k.eps) {   // nothing on the floor
+          Se = SU;
+          Ee = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) + 1e-14 * SU : 0.0;
+        } else if (have_y && hi < k.eps) {    // everything on the floor
+          Se = Y;
+          Ee = 1e-14 * Y;
+        } else {
+          Se = fmin(SUf, Yf) * (1.0 + 1e-6);  // an upper bound of the oracle's sum
+          if (!open && !amb) why = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
+          open = true;
+        }
+        // the next step's prediction, with a factor-2 margin on either side of the floor
+        const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
+        stg(&t.sc->regime, (bad || !finite) ? (int32_t)kRegimeBoth : (int32_t)next);
+      }
+    } else {
+      const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
+      Se = wg_sum(t.ssum, ntiles, sh);
+      const double Q4 = wg_sum(t.qsum, ntiles, sh);
+      // the exact second moment's sum is the oracle's own; a factored one carries the
+      // spread of its unrounded terms (20 standard deviations)
+      Ee = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) + 1e-14 * Se : 0.0;
     }
-    // the next step's prediction, with a factor-2 margin on either side of the floor
-    const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
-    stg(&t.sc->regime, (bad || !finite) ? (int32_t)kRegimeBoth : (int32_t)next);
+    if (threadIdx.x == 0) {
+      S += Se;
+      err += Ee;
+      stg(&t.sc->q, q);
+    }
+  }
+  if (threadIdx.x != 0) return;
+  int level = 2;   // the re-check a flagged group gets
+  double spread = 0.0;
+  if (bad_any) {
+    amb = true;
+    why = kWhyNonFinite;
+  } else if (open) {
+    S += err;   // an upper bound of the group's sum
+    if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
+      amb = true;
+      level = 1;   // the floor split per element decides most of these
+    }
   } else {
-    S = wg_sum(t.ssum, ntiles, sh);
-    const double Q4 = wg_sum(t.qsum, ntiles, sh);
-    if (threadIdx.x != 0) return;
-    // exact second moment: the sum is already the oracle's own
-    spread = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
+    spread = S > 0.0 ? err / S : 0.0;
   }
   const bool flagged_before = amb;
   const float kf = clip_from_sum(S, N, k.d, spread, amb);
   if (amb && !flagged_before) why = kWhySpread;
-  stg(&t.sc->k, kf);
-  stg(&t.sc->q, q);
-  if (amb && t.kind == kFactored) {
-    int32_t *list = recheck_list(L, ntensors, level);
-    const int pos = atomicAdd(level == 1 ? &L->n1 : &L->n2, 1);
-    stg(list + pos, (int32_t)it.tensor);
-    stg(&t.sc->ambiguous, (int32_t)((level == 1 ? kClipPending1 : kClipPending2) | (why << 4)));
-  } else {
-    stg(&t.sc->ambiguous, (int32_t)kClipFast);
+  const int pos = (amb && t0.kind == kFactored) ? atomicAdd(level == 1 ? &L->n1 : &L->n2, ng) : 0;
+  for (int e = 0; e < ng; e++) {
+    const DevTensor &t = TT[g0 + e];
+    stg(&t.sc->k, kf);
+    if (amb && t0.kind == kFactored) {
+      stg(recheck_list(L, ntensors, level) + pos + e, (int32_t)(g0 + e));
+      stg(&t.sc->ambiguous, (int32_t)((level == 1 ? kClipPending1 : kClipPending2) | (why << 4)));
+    } else {
+      stg(&t.sc->ambiguous, (int32_t)kClipFast);
+    }
   }
 }
 
@@ -1508,9 +1545,10 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
   const float alpha = (float)(c.lsk * ldg(t.ainv + i));
   // pairs p0 .. p0 + 3: m and col are multiples of 8, so p0 is a multiple of 4 and the
   // four pairs share their high word and differ only in the low two bits
-  const uint64_t p0 = ((uint64_t)i * (uint64_t)t.m + (uint64_t)col) >> 1;
+  const uint64_t p0 = ((uint64_t)t.idx0 + (uint64_t)i * (uint64_t)t.m + (uint64_t)col) >> 1;
   // pair indices reach 2^32 only in tensors of more than 2^33 elements (a uniform test)
-  const uint32_t base = (t.n * t.m > (int64_t(1) << 33)) ? dz.pair_base(p0) : ((uint32_t)p0 ^ dz.klo ^ dz.inner0);
+  const uint32_t base =
+      (t.idx0 + t.n * t.m > (int64_t(1) << 33)) ? dz.pair_base(p0) : ((uint32_t)p0 ^ dz.klo ^ dz.inner0);
   float y[8], dith[8];
 #pragma unroll
   for (int e2 = 0; e2 < 4; e2++) {
@@ -1579,7 +1617,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
     for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
     const int64_t i = tl.row(lr);
       const float alpha = (float)(c.lsk * ldg(t.ainv + i));
-      const uint64_t rowidx = (uint64_t)i * (uint64_t)m;
+      const uint64_t rowidx = (uint64_t)t.idx0 + (uint64_t)i * (uint64_t)m;
 #pragma unroll
       for (int e = 0; e < 8; e++) {
         if (col + e >= m) continue;
@@ -1632,7 +1670,7 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
       }
       const float U = __fmul_rn(num / dd, kc);
       const float x = fmaf(-k.lr, U, decayed(w, t.decay && k.wd != 0.f, k.wd));
-      const uint64_t idx = (uint64_t)sidx;
+      const uint64_t idx = (uint64_t)(t.idx0 + sidx);
       const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), fabsf(w), x);
       stg(t.w + i * ld + col + e, to_bf16(y));
     }

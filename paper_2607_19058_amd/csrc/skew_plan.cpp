@@ -15,20 +15,45 @@ static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   if (n < 0 || (n > 0 && d == nullptr) || out == nullptr) return SKEW_EINVAL;
   Plan p;
-  p.t.resize(n);
+  // descriptors -> sub-tensors: a stacked (ndim 3) descriptor of E matrices becomes E
+  // sub-tensors (one per slice, factored on its own, Sec. 3 footnote) that share one clip
+  // factor; every other descriptor is one sub-tensor
+  p.desc_sub0.assign((size_t)n, 0);
+  p.desc_nsub.assign((size_t)n, 1);
+  int64_t nsub = 0;
+  for (int i = 0; i < n; i++) {
+    const skew_tensor_desc &x = d[i];
+    if (x.tier < SKEW_TIER_BACKBONE || x.tier > SKEW_TIER_ROUTER) return SKEW_EINVAL;
+    if (x.ndim < 1 || x.ndim > 3) return SKEW_EINVAL;
+    if ((x.state_flags & ~(uint32_t)(SKEW_STATE_MOMENTUM | SKEW_STATE_FACTORED)) != 0) return SKEW_EINVAL;
+    if (x.ndim == 3 ? x.batch < 0 : (x.batch != 0 && x.batch != 1)) return SKEW_EINVAL;
+    const int64_t E = (x.ndim == 3 && x.batch > 1) ? x.batch : 1;
+    if (E > INT32_MAX / 4) return SKEW_EINVAL;
+    p.desc_sub0[(size_t)i] = (int32_t)nsub;
+    p.desc_nsub[(size_t)i] = (int32_t)E;
+    nsub += E;
+    if (nsub > INT32_MAX / 4) return SKEW_EINVAL;
+  }
+  p.t.resize((size_t)nsub);
   size_t st = 0;        // state bytes
   size_t ws_part = 0;   // partial-sum bytes (offsets relative to the partial region)
   int64_t items_total = 0;
-  for (int i = 0; i < n; i++) {
-    const skew_tensor_desc &x = d[i];
-    TensorPlan &tp = p.t[i];
-    if (x.tier < SKEW_TIER_BACKBONE || x.tier > SKEW_TIER_ROUTER) return SKEW_EINVAL;
-    if (x.ndim != 1 && x.ndim != 2) return SKEW_EINVAL;
+  for (int di = 0; di < n; di++) {
+  const skew_tensor_desc &x = d[di];
+  const int32_t sub0 = p.desc_sub0[(size_t)di], E = p.desc_nsub[(size_t)di];
+  for (int32_t e = 0; e < E; e++) {
+    const int i = sub0 + e;   // the sub-tensor
+    TensorPlan &tp = p.t[(size_t)i];
+    tp.desc = di;
+    tp.grp0 = sub0;
+    tp.ngrp = E;
     if (x.rows < 0 || x.cols < 0) return SKEW_EINVAL;
     if (x.rows > 0 && x.cols > INT64_MAX / x.rows) return SKEW_EINVAL;
-    const int64_t N = x.rows * x.cols;
+    const int64_t N = (x.ndim == 3 && x.batch == 0) ? 0 : x.rows * x.cols;
+    if (N > 0 && E > INT64_MAX / N) return SKEW_EINVAL;
     tp.tier = x.tier;
     tp.N = N;
+    tp.idx0 = (int64_t)e * N;   // the slice's first element in the stacked tensor
     if (x.ndim == 1) {
       if (N > 0 && x.rows != 1 && x.cols != 1) return SKEW_EINVAL;
       tp.n = N > 0 ? 1 : 0;
@@ -36,22 +61,35 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.ld = N;
     } else {
       if (x.ld < x.cols || x.ld < 1) return SKEW_EINVAL;
-      if (x.rows > 0 && x.ld > INT64_MAX / x.rows) return SKEW_EINVAL;
+      if (x.rows > 0 && x.ld > INT64_MAX / x.rows / E) return SKEW_EINVAL;
       tp.n = x.rows;
       tp.m = x.cols;
       tp.ld = x.ld;
     }
     tp.empty = (N == 0);
-    tp.kind = (x.tier == SKEW_TIER_ROUTER || x.ndim == 1) ? kExact : kFactored;
-    tp.momentum = (x.tier == SKEW_TIER_BACKBONE);
+    // tiers (Fig. 1) and their variants (Table 3): momentum in the backbone or on request;
+    // the exact second moment for vectors and router matrices unless factoring is requested
+    const bool factor_router = (x.state_flags & SKEW_STATE_FACTORED) != 0;
+    tp.kind = ((x.tier == SKEW_TIER_ROUTER && !factor_router) || x.ndim == 1) ? kExact : kFactored;
+    tp.momentum = (x.tier == SKEW_TIER_BACKBONE || (x.state_flags & SKEW_STATE_MOMENTUM) != 0) ? 1 : 0;
     if (tp.empty) continue;
 
-    // state slices
-    if (tp.momentum) { tp.off_m = st; st = align_up(st + (size_t)N * 4); }
-    if (tp.kind == kExact) { tp.off_v = st; st = align_up(st + (size_t)N * 4); }
-    if (tp.kind == kFactored) {
-      tp.off_r = st; st = align_up(st + (size_t)tp.n * 4);
-      tp.off_c = st; st = align_up(st + (size_t)tp.m * 4);
+    // state slices: one contiguous array per descriptor (slice e at e times the slice)
+    if (e == 0) {
+      if (tp.momentum) { tp.off_m = st; st = align_up(st + (size_t)E * N * 4); }
+      if (tp.kind == kExact) { tp.off_v = st; st = align_up(st + (size_t)E * N * 4); }
+      if (tp.kind == kFactored) {
+        tp.off_r = st; st = align_up(st + (size_t)E * tp.n * 4);
+        tp.off_c = st; st = align_up(st + (size_t)E * tp.m * 4);
+      }
+    } else {
+      const TensorPlan &t0 = p.t[(size_t)sub0];
+      if (tp.momentum) tp.off_m = t0.off_m + (size_t)e * N * 4;
+      if (tp.kind == kExact) tp.off_v = t0.off_v + (size_t)e * N * 4;
+      if (tp.kind == kFactored) {
+        tp.off_r = t0.off_r + (size_t)e * tp.n * 4;
+        tp.off_c = t0.off_c + (size_t)e * tp.m * 4;
+      }
     }
 
     // tile grid: tr rows x (512 * cw) columns, about kTileElems elements; cw in {1, 2, 4}
@@ -68,7 +106,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     tp.off_ssum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
     tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
     tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
-    p.clip.push_back({i, 0});
+    if (e == 0) p.clip.push_back({i, 0});   // one clip item per group (its first slice)
     // Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
     // row, nseg (1, 2 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
     // row and zrpi = 8 / wpr rows are side by side. A block of zrpi * zrb rows (bf16
@@ -128,13 +166,15 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     items_total += tiles;
     if (items_total > INT32_MAX / 2) return SKEW_EINVAL;
   }
+  }
+  const int nt = (int)p.t.size();   // sub-tensors: the device table's entries
   // pipeline groups: consecutive tensors, about equal algorithmic bytes (gradient, weight
   // read and write, and the state each tier reads and writes)
   {
-    std::vector<double> bytes(n, 0.0);
+    std::vector<double> bytes(nt, 0.0);
     double total = 0.0;
     int nonempty = 0;
-    for (int i = 0; i < n; i++) {
+    for (int i = 0; i < nt; i++) {
       const TensorPlan &tp = p.t[i];
       if (tp.empty) continue;
       bytes[i] = (double)tp.N * (6.0 + (tp.momentum ? 8.0 : 0.0) + (tp.kind == kExact ? 8.0 : 0.0));
@@ -142,9 +182,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       nonempty++;
     }
     p.ngroups = std::max(1, std::min(kMaxGroups, nonempty));
-    p.tgroup.assign(n, 0);
+    p.tgroup.assign(nt, 0);
     double acc = 0.0;
-    for (int i = 0; i < n; i++) {
+    for (int i = 0; i < nt; i++) {
       const int g = total > 0.0 ? (int)(acc / total * p.ngroups) : 0;
       p.tgroup[i] = std::min(g, p.ngroups - 1);
       acc += bytes[i];
@@ -153,18 +193,18 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   p.state_bytes = st;
   // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][re-check lists][partials]
   size_t ws = 0;
-  p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(n, 1));
+  p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(nt, 1));
   p.off_items = ws;
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
                                      p.clip.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
-  ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(n, 1));
+  ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
   p.off_zero = ws;   // zero-filled with the workspace at set-up and never written
   ws = align_up(ws + 256);
   p.off_gscale = ws;
   ws = align_up(ws + sizeof(float));
   p.off_gsq = ws;
-  ws = align_up(ws + sizeof(double) * (size_t)std::max(n, 1));
+  ws = align_up(ws + sizeof(double) * (size_t)std::max(nt, 1));
   auto shift = [ws](size_t &off) {
     if (off != SIZE_MAX) off += ws;
   };

@@ -17,8 +17,9 @@ LIB_PATH = os.path.join(HERE, "libskewadam.so")
 SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
 FLAG_EXACT_CLIP = 1
+STATE_MOMENTUM, STATE_FACTORED = 1, 2   # tier variants (SKEW_STATE_*)
 TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 # names every build of the library exports (checked by the CPU test suite)
 EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
@@ -38,6 +39,7 @@ class TensorDesc(ctypes.Structure):
         ("tensor_id", ctypes.c_uint64),
         ("w", ctypes.c_void_p), ("g", ctypes.c_void_p),
         ("m", ctypes.c_void_p), ("v", ctypes.c_void_p), ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
+        ("batch", ctypes.c_int64), ("state_flags", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
     ]
 
 
@@ -99,9 +101,9 @@ def _strerror(status: int) -> str:
 
 
 def make_desc(tier: int, ndim: int, rows: int, cols: int, ld: int, tensor_id: int, w_ptr: int = 0,
-              g_ptr: int = 0) -> TensorDesc:
+              g_ptr: int = 0, batch: int = 0, state_flags: int = 0) -> TensorDesc:
     return TensorDesc(tier, ndim, rows, cols, ld, tensor_id & (2**64 - 1), w_ptr or None, g_ptr or None,
-                      None, None, None, None)
+                      None, None, None, None, batch, state_flags, 0)
 
 
 def state_bytes(descs: Sequence[TensorDesc]):
@@ -114,7 +116,7 @@ def state_bytes(descs: Sequence[TensorDesc]):
     return sb.value, wb.value
 
 
-def _desc_for(tier: int, w, g, tensor_id: int) -> TensorDesc:
+def _desc_for(tier: int, w, g, tensor_id: int, state_flags: int = 0) -> TensorDesc:
     import torch
     if w.dtype != torch.bfloat16 or g.dtype != torch.bfloat16:
         raise TypeError("weights and gradients must be bfloat16")
@@ -125,20 +127,34 @@ def _desc_for(tier: int, w, g, tensor_id: int) -> TensorDesc:
     if w.dim() == 1:
         if w.numel() > 1 and w.stride(0) != 1:
             raise ValueError("vectors must be contiguous")
-        return make_desc(tier, 1, 1, w.shape[0], max(1, w.shape[0]), tensor_id, w.data_ptr(), g.data_ptr())
+        return make_desc(tier, 1, 1, w.shape[0], max(1, w.shape[0]), tensor_id, w.data_ptr(), g.data_ptr(),
+                         state_flags=state_flags)
+    if w.dim() == 3:
+        # stacked (E, n, m): slices at a stride of n * ld elements
+        E, n, m = w.shape
+        if m > 1 and w.stride(2) != 1:
+            raise ValueError("stacked matrices must be row-major (unit column stride)")
+        ld = w.stride(1) if n > 1 else max(1, m)
+        ld = max(ld, m, 1)
+        if E > 1 and w.stride(0) != n * ld:
+            raise ValueError("stacked slices must follow each other (slice stride rows * ld)")
+        return make_desc(tier, 3, n, m, ld, tensor_id, w.data_ptr(), g.data_ptr(), batch=E,
+                         state_flags=state_flags)
     if w.dim() != 2:
-        raise ValueError("only vectors and matrices are supported")
+        raise ValueError("only vectors, matrices and stacked matrices are supported")
     n, m = w.shape
     if m > 1 and w.stride(1) != 1:
         raise ValueError("matrices must be row-major (unit column stride)")
     ld = w.stride(0) if n > 1 else max(1, m)
-    return make_desc(tier, 2, n, m, max(ld, m, 1), tensor_id, w.data_ptr(), g.data_ptr())
+    return make_desc(tier, 2, n, m, max(ld, m, 1), tensor_id, w.data_ptr(), g.data_ptr(), state_flags=state_flags)
 
 
 class SkewAdam:
     """One SkewAdam context over a fixed set of (tier, weight, gradient) tensors.
 
-    ``params`` is a list of ``(tier, w, g, tensor_id)`` with bf16 CUDA/HIP tensors.
+    ``params`` is a list of ``(tier, w, g, tensor_id)`` or ``(tier, w, g, tensor_id,
+    state_flags)`` with bf16 CUDA/HIP tensors: vectors, matrices or stacked (E, n, m)
+    matrices; ``state_flags`` takes STATE_MOMENTUM / STATE_FACTORED (tier variants).
     The state and workspace are allocated here as torch byte tensors on the same
     device; weights, gradients and these buffers must outlive the object.
     """
@@ -147,7 +163,8 @@ class SkewAdam:
         import torch
         params = list(params)
         self._keep = params
-        self.descs = [_desc_for(TIERS.get(t, t), w, g, tid) for (t, w, g, tid) in params]
+        self.descs = [_desc_for(TIERS.get(p[0], p[0]), p[1], p[2], p[3], p[4] if len(p) > 4 else 0)
+                      for p in params]
         self.device = params[0][1].device if params else torch.device("cuda", torch.cuda.current_device())
         sb, wb = state_bytes(self.descs)
         self.state = torch.empty(max(sb, 1), dtype=torch.uint8, device=self.device)
@@ -211,7 +228,8 @@ class SkewAdam:
         import torch
         d = self._arr[i]
         n, m = (1, d.rows * d.cols) if d.ndim == 1 else (d.rows, d.cols)
-        shape = {"m": (n * m,), "v": (n * m,), "r": (n,), "c": (m,)}
+        E = d.batch if d.ndim == 3 else 1
+        shape = {"m": (E * n * m,), "v": (E * n * m,), "r": (E * n,), "c": (E * m,)}
         base = self.state.data_ptr()
         out = {}
         for name in ("m", "v", "r", "c"):

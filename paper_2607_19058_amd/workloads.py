@@ -47,7 +47,8 @@ class Spec:
     shape: tuple
     tensor_id: int
     bank: int = -1       # expert bank (routing group) or -1
-    expert: int = -1     # expert index within its bank or -1
+    expert: int = -1     # expert index within its bank (a stacked tensor: its first) or -1
+    state_flags: int = 0 # tier variant of the ablation (momentum / factored router)
 
     @property
     def numel(self) -> int:
@@ -154,7 +155,20 @@ def ragged() -> Workload:
     return Workload("ragged", specs, 50, banks={0: 64, 1: 64}, zero_per_step={0: 3, 1: 3})
 
 
-CONFIGS = {"tiny": tiny, "layer": layer, "full": full, "stress": stress, "ragged": ragged}
+def tiny_stacked() -> Workload:
+    """The tiny workload with each expert bank projection stacked into one (8, n, m) tensor."""
+    base = tiny()
+    specs = [s for s in base.specs if s.bank < 0]
+    nid = max(s.tensor_id for s in base.specs) + 1
+    for proj, shape in (("up", (8, 256, 1024)), ("down", (8, 256, 1024))):
+        specs.append(Spec(f"ex.{proj}", EXPERT, shape, nid, bank=0, expert=0))
+        nid += 1
+    return Workload("tiny_stacked", specs, 8, banks={0: 8}, fixed_zero=base.fixed_zero, redraw_shares=True,
+                    zero_per_step={0: 1})
+
+
+CONFIGS = {"tiny": tiny, "layer": layer, "full": full, "stress": stress, "ragged": ragged,
+           "tiny_stacked": tiny_stacked}
 
 
 def get(name: str) -> Workload:
@@ -206,10 +220,17 @@ def fill_grad(spec: Spec, wl: Workload, step: int, out, scales: Optional[Dict[in
     import torch
     if scales is None:
         scales = expert_scales(wl, step)
-    rho = 1.0 if spec.bank < 0 else float(scales[spec.bank][spec.expert])
-    if rho == 0.0:
-        out.zero_()
-        return out
+    stacked = len(spec.shape) == 3 and spec.bank >= 0   # slice e is expert `expert + e`
+    if stacked:
+        rho = scales[spec.bank][spec.expert:spec.expert + spec.shape[0]]
+        if not np.any(rho):
+            out.zero_()
+            return out
+    else:
+        rho = 1.0 if spec.bank < 0 else float(scales[spec.bank][spec.expert])
+        if rho == 0.0:
+            out.zero_()
+            return out
     dev = out.device
     gen = torch.Generator(device=dev)
     gen.manual_seed(_seed(wl.seed, 2, step, spec.tensor_id))
@@ -227,6 +248,9 @@ def fill_grad(spec: Spec, wl: Workload, step: int, out, scales: Optional[Dict[in
         keep = torch.rand(spec.shape, generator=gen, device=dev) >= wl.expert_sparsity
         z.mul_(keep)
         del keep
-    z.mul_(SIGMA_G * rho)
+    if stacked:
+        z.mul_(torch.as_tensor(SIGMA_G * rho, dtype=torch.float32, device=dev)[:, None, None])
+    else:
+        z.mul_(SIGMA_G * rho)
     out.copy_(z)
     return out

@@ -77,7 +77,8 @@ class ParityRun:
         self.specs = specs if specs is not None else wl.specs
         self.W = [W.init_weight(s, wl, self.device) for s in self.specs]
         self.G = [torch.zeros(s.shape, dtype=torch.bfloat16, device=self.device) for s in self.specs]
-        self.opt = SkewAdam([(s.tier, self.W[k], self.G[k], s.tensor_id) for k, s in enumerate(self.specs)])
+        self.opt = SkewAdam([(s.tier, self.W[k], self.G[k], s.tensor_id, s.state_flags)
+                             for k, s in enumerate(self.specs)])
         idx = list(range(len(self.specs))) if sample is None else list(sample)
         self.sample = idx
         self.O = {}
@@ -85,7 +86,8 @@ class ParityRun:
         for k in idx:
             s = self.specs[k]
             w = bits(self.W[k])
-            self.O[k] = oracle.Tensor(tier=s.tier, w=w.copy(), g=np.zeros_like(w), tensor_id=s.tensor_id).init_state()
+            self.O[k] = oracle.Tensor(tier=s.tier, w=w.copy(), g=np.zeros_like(w), tensor_id=s.tensor_id,
+                                      state_flags=s.state_flags).init_state()
             self.diverged[k] = np.zeros(w.shape, bool)
         self.stats = Stats()
 
@@ -139,7 +141,7 @@ class ParityRun:
                 assert name not in views, (s.name, name)
                 continue
             got = views[name].cpu().numpy().astype(np.float64)
-            r = ref.astype(np.float64)
+            r = ref.ravel().astype(np.float64)
             err = np.abs(got - r)
             lim = REL_STATE * np.abs(r)
             bad = int(np.count_nonzero(~(err <= lim)) - np.count_nonzero(np.isnan(got) & np.isnan(r)))

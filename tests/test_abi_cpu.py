@@ -26,7 +26,7 @@ def test_library_exports_every_declared_function():
     L = ctypes.CDLL(P.skewadam.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
-    assert P.lib().skew_abi_version() == P.skewadam.ABI_VERSION == 2
+    assert P.lib().skew_abi_version() == P.skewadam.ABI_VERSION == 3
     for code in (0, -1, -2, -3, -4, -99):
         assert P.lib().skew_strerror(code)
 
@@ -79,6 +79,54 @@ def test_paper_inventory_state_bytes():
     assert round(sb / 2**30, 2) == 1.29      # Table 1, Table 6
 
 
+def _inventory():
+    inv = []
+    for line in open(os.path.join(ROOT, "tests", "golden", "paper_model_inventory.txt")):
+        line = line.split("|")[0].strip()
+        if line and not line.startswith("#"):
+            tier, count, shape = line.split()
+            inv += [(oracle.TIER_NAMES[tier], tuple(int(x) for x in shape.split("x")))] * int(count)
+    return inv
+
+
+@pytest.mark.parametrize("policy", ["skewadam", "expert_momentum", "factored_router", "uniform"])
+def test_tier_variants_state_bytes(policy):
+    """The library's state for each row of the tier ablation (Table 3) equals the closed
+    form, which the memory tests pin to the table's 1.29 / 25.29 / 1.28 / 25.29 GB."""
+    flags = {"skewadam": {}, "expert_momentum": {W.EXPERT: P.STATE_MOMENTUM},
+             "factored_router": {W.ROUTER: P.STATE_FACTORED},
+             "uniform": {t: P.STATE_MOMENTUM | P.STATE_FACTORED for t in (W.BACKBONE, W.EXPERT, W.ROUTER)}}[policy]
+    inv = _inventory()
+    descs = []
+    for k, (t, s) in enumerate(inv):
+        f = flags.get(t, 0)
+        if len(s) == 1:
+            descs.append(P.make_desc(t, 1, 1, s[0], s[0], k, state_flags=f))
+        else:
+            descs.append(P.make_desc(t, 2, s[0], s[1], s[1], k, state_flags=f))
+    sb, _ = P.state_bytes(descs)
+    closed = oracle.state_bytes(inv, policy)
+    assert closed <= sb <= closed + 256 * 3 * len(inv)
+
+
+def test_stacked_state_bytes_equal_separate_matrices():
+    """A stacked (E, n, m) tensor keeps E slices' state: the same bytes as E matrices."""
+    for tier in (W.BACKBONE, W.EXPERT, W.ROUTER):
+        E, n, m = 128, 64, 96
+        sb_st, _ = P.state_bytes([P.make_desc(tier, 3, n, m, m, 0, batch=E)])
+        sb_sep, _ = P.state_bytes([P.make_desc(tier, 2, n, m, m, k) for k in range(E)])
+        closed = E * oracle.tensor_state_floats(tier, (n, m)) * 4
+        assert closed <= sb_st <= closed + 256 * 3
+        assert closed <= sb_sep
+
+
+def test_stacked_2p31_descriptor_is_accepted():
+    """A stacked tensor of 2^31 elements (the 8-bit optimizers' limit, Sec. 3 footnote)
+    plans with 64-bit sizes: 128 x 4096 x 4096."""
+    sb, wb = P.state_bytes([P.make_desc(W.EXPERT, 3, 4096, 4096, 4096, 0, batch=128)])
+    assert sb >= 128 * (4096 + 4096) * 4 and wb > 0
+
+
 def _rc(descs):
     arr = (P.TensorDesc * max(1, len(descs)))(*descs)
     a, b = ctypes.c_size_t(), ctypes.c_size_t()
@@ -90,7 +138,12 @@ def test_validation_errors():
     assert _rc([ok]) == 0
     assert _rc([P.make_desc(3, 2, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL        # unknown tier
     assert _rc([P.make_desc(-1, 2, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL
-    assert _rc([P.make_desc(1, 3, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL        # ndim 3
+    assert _rc([P.make_desc(1, 4, 4, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL        # ndim 4
+    assert _rc([P.make_desc(1, 3, 4, 8, 8, 0, batch=-1)]) == P.skewadam.SKEW_EINVAL   # negative batch
+    assert _rc([P.make_desc(1, 2, 4, 8, 8, 0, batch=2)]) == P.skewadam.SKEW_EINVAL    # batch on a matrix
+    assert _rc([P.make_desc(1, 2, 4, 8, 8, 0, state_flags=4)]) == P.skewadam.SKEW_EINVAL  # unknown flag
+    assert _rc([P.make_desc(1, 3, 4, 8, 8, 0, batch=0)]) == 0                        # no elements
+    assert _rc([P.make_desc(1, 3, 4, 8, 8, 0, batch=3)]) == 0
     assert _rc([P.make_desc(1, 2, 4, 8, 7, 0)]) == P.skewadam.SKEW_EINVAL        # ld < cols
     assert _rc([P.make_desc(1, 2, -1, 8, 8, 0)]) == P.skewadam.SKEW_EINVAL       # negative rows
     assert _rc([P.make_desc(1, 1, 2, 3, 3, 0)]) == P.skewadam.SKEW_EINVAL        # vector that is 2x3

@@ -134,3 +134,86 @@ def test_new_hparam_errors_launch_nothing():
             opt.step(1, **bad)
     torch.cuda.synchronize()
     assert torch.equal(w, torch.ones_like(w))
+
+
+# ----------------------------------------------------------------------------- tier variants
+def _with_flags(wl, flags_by_tier):
+    import dataclasses
+    specs = [dataclasses.replace(s, state_flags=flags_by_tier.get(s.tier, 0)) for s in wl.specs]
+    return W.Workload(wl.name, specs, wl.steps, grad_kind=wl.grad_kind, seed=wl.seed, banks=wl.banks,
+                      zero_per_step=wl.zero_per_step, fixed_zero=wl.fixed_zero,
+                      expert_sparsity=wl.expert_sparsity, outlier_rate=wl.outlier_rate,
+                      outlier_scale=wl.outlier_scale, redraw_shares=wl.redraw_shares)
+
+
+VARIANTS = {
+    "expert_momentum": {W.EXPERT: oracle.STATE_MOMENTUM},
+    "factored_router": {W.ROUTER: oracle.STATE_FACTORED},
+    "uniform": {t: oracle.STATE_MOMENTUM | oracle.STATE_FACTORED for t in (W.BACKBONE, W.EXPERT, W.ROUTER)},
+}
+
+
+@pytest.mark.parametrize("variant", sorted(VARIANTS))
+def test_variants_tiny_every_tensor(variant):
+    log(f"[parity] tiny, tier variant {variant}: 21 tensors, 6 steps, all compared")
+    st = run(_with_flags(W.get("tiny"), VARIANTS[variant]), steps=6)
+    assert st.ok(), st
+
+
+def test_variants_unit_shapes_with_gradnorm():
+    log("[parity] unit shapes, uniform variant, gradient norm and decay, 3 steps")
+    st = run(_with_flags(_unit_workload(), VARIANTS["uniform"]),
+             hp=dict(oracle.DEFAULTS, lr=1e-2, weight_decay=2.0, max_grad_norm=0.05))
+    assert st.ok(), st
+
+
+def test_variant_expert_momentum_layer_sampled():
+    wl = _with_flags(W.get("layer"), VARIANTS["expert_momentum"])
+    names = {s.name: s.tensor_id for s in wl.specs}
+    sample = [names["attn.0"], names["ex3.up"], names["ex100.down"], names["router"]]
+    log(f"[parity] layer, momentum on experts: 263 tensors, 3 steps, sampled {sample}")
+    st = run(wl, steps=3, sample=sample)
+    assert st.ok(), st
+
+
+# ----------------------------------------------------------------------------- stacked tensors
+@pytest.mark.parametrize("hp", [oracle.DEFAULTS, BOTH], ids=["plain", "gnorm+decay"])
+def test_stacked_tiny_every_tensor(hp):
+    log(f"[parity] tiny with stacked (8, 256, 1024) expert tensors, {hp}, 8 steps, all compared")
+    st = run(W.get("tiny_stacked"), hp=hp)
+    assert st.ok(), st
+
+
+def test_stacked_exact_clip_everywhere():
+    from paper_2607_19058_amd.skewadam import FLAG_EXACT_CLIP
+    log("[parity] tiny stacked with the exact clip re-check forced")
+    st = run(W.get("tiny_stacked"), steps=4, flags=FLAG_EXACT_CLIP)
+    assert st.ok(), st
+
+
+def test_stacked_clip_factor_is_shared():
+    """skew_clip_info reports one clip factor per descriptor: a stacked tensor's slices
+    share it (their parity with the oracle, whose clip runs over the whole tensor, is
+    checked above)."""
+    dev = torch.device("cuda")
+    wl = W.get("tiny_stacked")
+    Wt = [W.init_weight(s, wl, dev) for s in wl.specs]
+    G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
+    opt = SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+    sc = W.expert_scales(wl, 1)
+    for k, s in enumerate(wl.specs):
+        W.fill_grad(s, wl, 1, G[k], sc)
+    opt.step(1)
+    kk, route = opt.clip_info()
+    assert len(kk) == len(wl.specs)
+    assert all(0.0 < x <= 1.0 for x in kk)
+
+
+def test_stacked_more_than_2p31_elements():
+    """A stacked expert tensor of 129 x 4096 x 4096 = 2,164,260,864 elements (> 2^31, the
+    size at which 8-bit optimizer kernels stop, Sec. 3 footnote), every element compared."""
+    wl = W.Workload("stacked_big", [W.Spec("ex", W.EXPERT, (129, 4096, 4096), 0)], 2)
+    log("[parity] stacked 129x4096x4096 expert tensor, 2 steps")
+    st = run(wl)
+    assert st.ok(), st
+    assert st.compared >= 2 * 129 * 4096 * 4096

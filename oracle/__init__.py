@@ -25,8 +25,9 @@ TIER_NAMES = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
 # Paper defaults (Alg. 1 caption, Table 5): beta = (0.9, 0.999), eps = 1e-8,
 # lr = 3e-4; update clipping at RMS 1 (Sec. 3).
 DEFAULTS = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0)
-# tier variants of the ablation (Table 3): momentum in any tier; router matrices factored
-STATE_MOMENTUM, STATE_FACTORED = 1, 2
+# tier variants of the ablation (Table 3): momentum in any tier; router matrices factored;
+# float32 master weights and gradients for exact-moment tensors (fp32 router and norms)
+STATE_MOMENTUM, STATE_FACTORED, STATE_FP32 = 1, 2, 4
 
 
 def build(verbose: bool = False) -> str:
@@ -60,6 +61,7 @@ class _HParams(ctypes.Structure):
         ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float),
         ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
         ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float), ("gsq_total", ctypes.c_double),
+        ("exact_ulp", ctypes.c_int32),
     ]
 
 
@@ -157,13 +159,14 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
          beta1: float = DEFAULTS["beta1"], beta2: float = DEFAULTS["beta2"], eps: float = DEFAULTS["eps"],
          clip_threshold: float = DEFAULTS["clip_threshold"], want_u: bool = False, want_x: bool = False,
          want_y: bool = False, weight_decay: float = 0.0, max_grad_norm: float = 0.0,
-         gsq_total: Optional[float] = None) -> int:
+         gsq_total: Optional[float] = None, exact_ulp: bool = False) -> int:
     """Run one oracle step over ``tensors`` in place. Returns the C status.
 
     weight_decay: lambda of the decoupled decay (router tier exempt). max_grad_norm > 0
     scales every gradient by min(1, max_grad_norm / (||G|| + 1e-6)) over all the tensors
     given, or over a larger set whose sum of squares is ``gsq_total``. The scale used is
-    returned by ``last_gcoef()``."""
+    returned by ``last_gcoef()``. exact_ulp: the dither spans the exact bf16 ulp of w.
+    Tensors with STATE_FP32 hold float32 w and g (the arrays' dtype) and skip the cast."""
     tensors = list(tensors)
     arr = (_Tensor * max(1, len(tensors)))()
     rms = np.full(max(1, len(tensors)), np.nan, np.float64)
@@ -173,7 +176,8 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
             a = getattr(t, name)
             if a is not None:
                 assert a.flags["C_CONTIGUOUS"], name
-        assert t.w.dtype == np.uint16 and t.g.dtype == np.uint16 and t.w.shape == t.g.shape
+        want = np.float32 if t.state_flags & STATE_FP32 else np.uint16
+        assert t.w.dtype == want and t.g.dtype == want and t.w.shape == t.g.shape
         n, m = t.rows_cols
         E = t.batch
         if n * m > 0:
@@ -194,7 +198,7 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
                          rms.ctypes.data + 8 * k, E if t.ndim == 3 else 0, int(t.state_flags))
         keep.append(t)
     hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1),
-                  weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total))
+                  weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total), int(exact_ulp))
     gc = ctypes.c_float(0.0)
     rc = lib().skew_oracle_step_gcoef(ctypes.byref(hp), arr, len(tensors), ctypes.byref(gc))
     global _LAST_GCOEF

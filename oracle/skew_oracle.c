@@ -53,13 +53,30 @@ typedef struct {
   int gclip;      /* gradient-norm scaling on */
   float gcoef;    /* the gradient scale c (1 when off) */
   double gc2;     /* c * c, exact in double */
+  int exact_ulp;  /* dither width from the exact bf16 ulp of w */
 } consts_t;
+
+/* a gradient or weight element: bf16 bits, or float32 for float32 masters */
+static float elem_f32(const void *p, int64_t idx, int fp32);
 
 static float bf16_bits_to_f32(uint16_t b) {
   uint32_t u = (uint32_t)b << 16;
   float f;
   memcpy(&f, &u, sizeof f);
   return f;
+}
+
+static float elem_f32(const void *p, int64_t idx, int fp32) {
+  return fp32 ? ((const float *)p)[idx] : bf16_bits_to_f32(((const uint16_t *)p)[idx]);
+}
+
+/* the spacing of bf16 values around w: 2^(E - 134) for biased exponent E >= 1 (8 bits of
+ * significand), 2^-133 among the subnormals; exact in float */
+static float bf16_ulp(float w) {
+  uint32_t u;
+  memcpy(&u, &w, sizeof u);
+  const int E = (int)((u >> 23) & 0xFF);
+  return ldexpf(1.0f, (E >= 1 ? E : 1) - 134);
 }
 
 /* round-to-nearest, ties-to-even, from float32 to the upper 16 bits; NaN -> 0x7FC0 */
@@ -173,6 +190,7 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
   const int64_t n1 = T->rows, m = T->cols, n = E * n1, N = n * m;
   if (n1 <= 0 || m <= 0) return;
   const int exact = (T->tier == ORACLE_ROUTER && !(T->state_flags & ORACLE_STATE_FACTORED)) || (T->ndim == 1);
+  const int fp32 = (T->state_flags & ORACLE_STATE_FP32) != 0;   /* float32 w and g (exact tensors) */
   const int momentum = (T->tier == ORACLE_BACKBONE) || (T->state_flags & ORACLE_STATE_MOMENTUM);
   float *uhat = (float *)malloc((size_t)N * sizeof(float));
   double *row_ss = (double *)malloc((size_t)n * sizeof(double));
@@ -181,7 +199,7 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
   if (!exact) {
     cprime = (float *)malloc((size_t)(E * m) * sizeof(float));
     for (int64_t e = 0; e < E; e++)
-      factored_stats(K, T->g + e * n1 * m, T->r + e * n1, T->c + e * m, n1, m, cprime + e * m);
+      factored_stats(K, (const uint16_t *)T->g + e * n1 * m, T->r + e * n1, T->c + e * m, n1, m, cprime + e * m);
   }
 
   /* preconditioned update and its sum of squares, row by row */
@@ -190,7 +208,7 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
     double s = 0.0;
     for (int64_t j = 0; j < m; j++) {
       const int64_t idx = i * m + j;
-      float g = bf16_bits_to_f32(T->g[idx]);
+      float g = elem_f32(T->g, idx, fp32);
       if (K->gclip) g = K->gcoef * g;   /* the scaled gradient, rounded once */
       float dd;
       if (exact) {
@@ -228,18 +246,28 @@ static void step_tensor(const consts_t *K, skew_oracle_tensor *T) {
   const int decay = K->wd != 0.0f && T->tier != ORACLE_ROUTER;
 #pragma omp parallel for schedule(static)
   for (int64_t idx = 0; idx < N; idx++) {
-    const float w = bf16_bits_to_f32(T->w[idx]);
+    const float w = elem_f32(T->w, idx, fp32);
     const float U = uhat[idx] * kclip;
     /* decoupled weight decay, w - (lr lambda) w with one rounding, ahead of the update */
     const float wdec = decay ? fmaf(-K->wd, w, w) : w;
     const float x = fmaf(-K->lr, U, wdec);
-    const int32_t e = 2 * (int32_t)skew_oracle_u16(key, (uint64_t)idx) + 1 - 65536;
-    const float f = (float)e * 0x1p-24f;
-    const float y = fmaf(f, fabsf(w), x);
     if (T->u_out) T->u_out[idx] = U;
     if (T->x_out) T->x_out[idx] = x;
+    if (fp32) {   /* float32 master: no cast, no dither */
+      if (T->y_out) T->y_out[idx] = x;
+      ((float *)T->w)[idx] = x;
+      continue;
+    }
+    const int32_t e = 2 * (int32_t)skew_oracle_u16(key, (uint64_t)idx) + 1 - 65536;
+    float y;
+    if (K->exact_ulp) {
+      /* xi = (e * 2^-17) * ulp(w), uniform on +-ulp(w)/2 on a 2^-16 grid; the product is exact */
+      y = fmaf((float)e * 0x1p-17f, bf16_ulp(w), x);
+    } else {
+      y = fmaf((float)e * 0x1p-24f, fabsf(w), x);
+    }
     if (T->y_out) T->y_out[idx] = y;
-    T->w[idx] = skew_oracle_f32_to_bf16(y);
+    ((uint16_t *)T->w)[idx] = skew_oracle_f32_to_bf16(y);
   }
   free(cprime);
   free(row_ss);
@@ -252,6 +280,10 @@ int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n
 
 int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n, float *gcoef_out) {
   if (hp->step < 1) return -1;
+  for (int i = 0; i < n; i++) {
+    const int exact = (t[i].tier == ORACLE_ROUTER && !(t[i].state_flags & ORACLE_STATE_FACTORED)) || t[i].ndim == 1;
+    if ((t[i].state_flags & ORACLE_STATE_FP32) && !exact) return -2;
+  }
   consts_t K;
   const double b1 = hp->beta1, b2 = hp->beta2, tt = (double)hp->step;
   K.b1 = hp->beta1;
@@ -266,6 +298,7 @@ int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t,
   K.step = hp->step;
   K.seed = hp->seed;
   K.wd = (float)((double)hp->lr * (double)hp->weight_decay);
+  K.exact_ulp = hp->exact_ulp != 0;
   K.gclip = hp->max_grad_norm > 0.0f;
   K.gcoef = 1.0f;
   if (K.gclip) {
@@ -275,7 +308,7 @@ int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t,
       const int64_t E = (t[i].ndim == 3 && t[i].batch > 0) ? t[i].batch : 1;
       const int64_t N = E * t[i].rows * t[i].cols;
       for (int64_t idx = 0; idx < N; idx++) {
-        const double gv = bf16_bits_to_f32(t[i].g[idx]);
+        const double gv = elem_f32(t[i].g, idx, (t[i].state_flags & ORACLE_STATE_FP32) != 0);
         total += gv * gv;
       }
     }

@@ -25,8 +25,8 @@ typedef struct {
   int32_t ndim;       /* 1 = vector, 2 = matrix */
   int64_t rows, cols; /* dense row-major, rows*cols elements */
   uint64_t tensor_id; /* keys the dither */
-  uint16_t *w;        /* bf16 bits, updated in place */
-  const uint16_t *g;  /* bf16 bits */
+  void *w;            /* bf16 bits (float with ORACLE_STATE_FP32), updated in place */
+  const void *g;      /* bf16 bits (float with ORACLE_STATE_FP32) */
   float *m;           /* momentum [rows*cols] (backbone) or NULL */
   float *v;           /* exact second moment [rows*cols] (router, vectors) or NULL */
   float *r;           /* factored row statistic [rows] or NULL */
@@ -41,8 +41,10 @@ typedef struct {
   uint32_t state_flags; /* ORACLE_STATE_*: tier variants of the ablation (Table 3) */
 } skew_oracle_tensor;
 
-/* Tier variants (Table 3): momentum kept in any tier; router matrices factored. */
-enum { ORACLE_STATE_MOMENTUM = 1, ORACLE_STATE_FACTORED = 2 };
+/* Tier variants (Table 3): momentum kept in any tier; router matrices factored; float32
+ * master weights and gradients (w, g point at float) for exact-moment tensors, updated in
+ * float32 without the dithered cast (the paper's fp32 router and norms, Sec. 4, Table 5). */
+enum { ORACLE_STATE_MOMENTUM = 1, ORACLE_STATE_FACTORED = 2, ORACLE_STATE_FP32 = 4 };
 
 typedef struct {
   float lr, beta1, beta2, eps, clip_threshold;
@@ -54,10 +56,13 @@ typedef struct {
                            min(1, max_grad_norm / (||G||_2 + 1e-6)) (Sec. 4); 0: off */
   double gsq_total;     /* < 0: ||G||_2^2 is summed over the n tensors given; >= 0: its value
                            (a step over a sample of a larger set passes the set's sum) */
+  int32_t exact_ulp;    /* 1: the dither spans the exact bf16 ulp of w, xi ~ U(+-ulp(w)/2), in
+                           place of the approximation ulp(w) ~ 2^-7 |w| (Sec. 3) */
 } skew_oracle_hparams;
 
-/* One step over n tensors. Returns 0, or -1 when step < 1. When gcoef_out is not NULL it
- * receives the gradient scale of the step (1 without max_grad_norm). */
+/* One step over n tensors. Returns 0, -1 when step < 1, -2 when a tensor asks for float32
+ * masters but keeps a factored second moment. When gcoef_out is not NULL it receives the
+ * gradient scale of the step (1 without max_grad_norm). */
 int skew_oracle_step(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n);
 int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t, int n, float *gcoef_out);
 

@@ -315,3 +315,79 @@ def test_stacked_clip_runs_over_the_whole_tensor():
     oracle.step([S], 1, clip_threshold=0.5, want_u=True)
     rms_after = float(np.sqrt(np.mean(S.u_out.astype(np.float64) ** 2)))
     assert S.rms > 0.5 and abs(rms_after - 0.5) <= 1e-6     # one factor k for all slices
+
+
+# ----------------------------------------------------------------------------- exact-ulp dither
+def _bf16_next(bits):
+    return bits + 1   # positive finite bf16: the next value up
+
+
+def test_exact_ulp_dither_keeps_grid_points():
+    """With the exact ulp the noise stays strictly inside +-ulp(w)/2, so a weight with a zero
+    update rounds back to itself (off powers of two, where the spacing below is half)."""
+    rng = np.random.default_rng(51)
+    w0 = bf16(rng.normal(0, 0.02, (64, 64)))
+    pow2 = (w0 & 0x7F) == 0
+    assert pow2.any()
+    w0[pow2] += 1                                          # off exact powers of two
+    T = make(E, w0)
+    oracle.step([T], 1, exact_ulp=True)                    # zero gradients: U = 0
+    assert np.array_equal(T.w, w0)
+    T2 = make(E, w0)
+    oracle.step([T2], 1)                                   # the approximate width moves some
+    assert not np.array_equal(T2.w, w0)
+
+
+@pytest.mark.parametrize("frac", [0.1, 0.37, 0.5, 0.83])
+def test_exact_ulp_dither_is_unbiased_stochastic_rounding(frac):
+    """Unbiased stochastic rounding (Sec. 3): with the exact ulp, a pre-cast value at
+    fraction f of the way between two bf16 neighbours rounds up with probability f."""
+    n = 1 << 15
+    lo_bits = np.full(n, 0x3C81, np.uint16)                # 2^-6 (1 + 2^-7): spacing 2^-13 either side
+    lo = float(f32(lo_bits[:1])[0])
+    ulp = 2.0 ** -13
+    # backbone vector (exact V), t = 1: U = sign(g); choose lr so that x = w + frac * ulp
+    T = make(B, lo_bits + np.uint16(1))                    # w one step up, x lands below it
+    T.g = bf16(np.full(n, 1e-2))
+    lr = (1.0 - frac) * ulp
+    oracle.step([T], 1, lr=lr, clip_threshold=float("inf"), want_x=True, exact_ulp=True)
+    x = T.x_out.astype(np.float64)
+    f_emp = float(np.mean((x - lo) / ulp))
+    assert abs(f_emp - frac) < 2e-3
+    up = np.mean(T.w == lo_bits + np.uint16(1))
+    assert np.all((T.w == lo_bits) | (T.w == lo_bits + np.uint16(1)))
+    assert abs(up - f_emp) < 4.0 * np.sqrt(f_emp * (1 - f_emp) / n) + 1e-3
+
+
+# ----------------------------------------------------------------------------- float32 masters
+def test_fp32_master_vector_is_adamw():
+    """Float32 master weights (the paper's fp32 norms and router, Table 5) are updated in
+    float32 with no cast: a backbone vector follows AdamW to float32 accuracy."""
+    rng = np.random.default_rng(61)
+    shape = (48,)
+    w0 = rng.normal(0, 0.02, shape).astype(np.float32)
+    T = oracle.Tensor(tier=B, w=w0.copy(), g=np.zeros(shape, np.float32), tensor_id=2,
+                      state_flags=oracle.STATE_FP32).init_state()
+    p = torch.tensor(w0.astype(np.float64), requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=LR, betas=(B1, B2), eps=0.0, weight_decay=0.05, foreach=False)
+    for t in range(1, 7):
+        g = rng.normal(0, 1e-2, shape).astype(np.float32) + 1e-4
+        T.g = g
+        with torch.no_grad():
+            p.copy_(torch.from_numpy(T.w.astype(np.float64)))
+        p.grad = torch.from_numpy(g.astype(np.float64))
+        opt.step()
+        oracle.step([T], t, eps=1e-30, clip_threshold=float("inf"), weight_decay=0.05)
+        np.testing.assert_allclose(T.w, p.detach().numpy(), rtol=3e-7, atol=1e-10)
+
+
+def test_fp32_master_router_matrix_and_factored_refusal():
+    rng = np.random.default_rng(62)
+    T = oracle.Tensor(tier=R, w=rng.normal(0, 0.02, (8, 4)).astype(np.float32), g=np.zeros((8, 4), np.float32),
+                      tensor_id=3, state_flags=oracle.STATE_FP32).init_state()
+    T.g = rng.normal(0, 1e-2, (8, 4)).astype(np.float32)
+    w_before = T.w.copy()
+    assert oracle.step([T], 1) == 0 and not np.array_equal(T.w, w_before)
+    F = oracle.Tensor(tier=E, w=np.zeros((8, 4), np.float32), g=np.zeros((8, 4), np.float32), tensor_id=4,
+                      state_flags=oracle.STATE_FP32).init_state()
+    assert oracle.step([F], 1) == -2

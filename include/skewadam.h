@@ -47,14 +47,17 @@ enum {
 
 enum { SKEW_TIER_BACKBONE = 0, SKEW_TIER_EXPERT = 1, SKEW_TIER_ROUTER = 2 };
 
-enum { SKEW_FLAG_EXACT_CLIP = 1 };
+enum { SKEW_FLAG_EXACT_CLIP = 1, SKEW_FLAG_EXACT_ULP = 2 };
 
 /* Per-tensor state variants (the tier ablation, Table 3): SKEW_STATE_MOMENTUM keeps fp32
  * momentum in any tier (then the bias correction of the backbone applies);
  * SKEW_STATE_FACTORED gives router matrices the factored second moment. Vectors always
  * keep the exact one (Alg. 1). "+ momentum on experts" is MOMENTUM on the expert tensors,
- * "factored router" FACTORED on the router, "uniform" both on every tensor. */
-enum { SKEW_STATE_MOMENTUM = 1, SKEW_STATE_FACTORED = 2 };
+ * "factored router" FACTORED on the router, "uniform" both on every tensor.
+ * SKEW_STATE_FP32: w and g are float32 (the paper's fp32 norms and router, Table 5),
+ * updated in float32 with no dither and no cast; only for tensors with the exact second
+ * moment (vectors, unfactored router matrices), else SKEW_EINVAL. */
+enum { SKEW_STATE_MOMENTUM = 1, SKEW_STATE_FACTORED = 2, SKEW_STATE_FP32 = 4 };
 
 /* One parameter tensor (Sec. 3 "The tiers": the policy assigns state by parameter role).
  *   tier      SKEW_TIER_*.
@@ -70,8 +73,9 @@ enum { SKEW_STATE_MOMENTUM = 1, SKEW_STATE_FACTORED = 2 };
  *   ld        row stride in elements, >= cols (ignored for vectors).
  *   tensor_id caller-chosen, stable across runs and checkpoints; keys the dither, so
  *             two tensors should not share an id.
- *   w         device, bf16 [rows x ld], read and written in place by skew_step.
- *   g         device, bf16 [rows x ld], read only.
+ *   w         device, bf16 [rows x ld] (float32 with SKEW_STATE_FP32), read and written in
+ *             place by skew_step.
+ *   g         device, bf16 [rows x ld] (float32 with SKEW_STATE_FP32), read only.
  *   m, v, r, c  OUT: filled by skew_state_init with pointers into the caller's state
  *             buffer (NULL where the tier keeps no such state); dense, row-major:
  *             m, v [rows*cols] (element (i, j) at i*cols + j), r [rows], c [cols];
@@ -105,9 +109,13 @@ typedef struct skew_tensor_desc {
  *   eps             > 0: floor of the second moment, and of mean(R) in the
  *                   factored reconstruction.
  *   clip_threshold  d > 0 (may be +inf: no clipping): U <- U / max(1, RMS(U)/d).
- *   flags           0, or SKEW_FLAG_EXACT_CLIP: always recompute the sum of squares behind
+ *   flags           0 or a combination of:
+ *                   SKEW_FLAG_EXACT_CLIP: always recompute the sum of squares behind
  *                   the clip factor with the reference float sequence (by default it is
- *                   recomputed only when a faster estimate cannot decide its rounding).
+ *                   recomputed only when a faster estimate cannot decide its rounding);
+ *                   SKEW_FLAG_EXACT_ULP: the dither spans the exact bf16 ulp of w,
+ *                   xi = (e 2^-17) ulp(w), in place of the approximation ulp(w) ~ 2^-7 |w|
+ *                   of Sec. 3: unbiased stochastic rounding.
  *   step            t >= 1, the caller's step counter (the library keeps none).
  *   seed            dither seed; with (step, tensor_id, element index) it fixes
  *                   every dither value, so results are bit-reproducible.

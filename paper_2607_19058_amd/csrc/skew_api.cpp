@@ -86,7 +86,7 @@ StepConsts make_consts(const skew_hparams &hp) {
 
 bool hparams_ok(const skew_hparams *hp) {
   if (hp == nullptr) return false;
-  if ((hp->flags & ~SKEW_FLAG_EXACT_CLIP) != 0 || hp->step < 1) return false;
+  if ((hp->flags & ~(SKEW_FLAG_EXACT_CLIP | SKEW_FLAG_EXACT_ULP)) != 0 || hp->step < 1) return false;
   if (!std::isfinite(hp->lr)) return false;
   if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f)) return false;
   if (!(hp->beta2 >= 0.0f && hp->beta2 < 1.0f)) return false;
@@ -152,10 +152,12 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     const TensorPlan &tp = p.t[i];
     if (tp.empty) continue;
     const skew_tensor_desc &dd = d[tp.desc];
-    const int64_t slice = (int64_t)(i - tp.grp0) * tp.n * tp.ld;   // elements to this slice's first row
+    // bytes to this slice's first row (elements of 2 bytes, or 4 for float32 masters)
+    const int64_t slice = (int64_t)(i - tp.grp0) * tp.n * tp.ld * (tp.fp32 ? 4 : 2);
     DevTensor &x = table[i];
-    x.w = static_cast<uint16_t *>(dd.w) + slice;
-    x.g = static_cast<const uint16_t *>(dd.g) + slice;
+    x.w = reinterpret_cast<uint16_t *>(static_cast<char *>(dd.w) + slice);
+    x.g = reinterpret_cast<const uint16_t *>(static_cast<const char *>(dd.g) + slice);
+    x.fp32 = tp.fp32;
     x.M = sp(tp.off_m);
     x.V = sp(tp.off_v);
     x.R = sp(tp.off_r);
@@ -194,7 +196,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.kind = tp.kind;
     x.decay = tp.tier != SKEW_TIER_ROUTER ? 1 : 0;
     x.momentum = tp.momentum;
-    x.vec = aligned16(x.w) && aligned16(x.g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
+    x.vec = !tp.fp32 && aligned16(x.w) && aligned16(x.g) && (tp.ld % 8 == 0) && (tp.m % 8 == 0);
     x.tensor_id = dd.tensor_id;
   }
   // row-band pass items by kernel variant (16-byte aligned rows or element loads is known

@@ -125,7 +125,9 @@ struct DevTensor {
   int64_t zrows;
   int64_t idx0;           // element index of this (sub-)tensor's first element in the caller's
                           // tensor: a stacked tensor's slices are sub-tensors (dither index)
-  int32_t grp0, ngrp;     // the sub-tensors that share one clip factor: [grp0, grp0 + ngrp)          // row-band pass: rows per band
+  int32_t grp0, ngrp;     // the sub-tensors that share one clip factor: [grp0, grp0 + ngrp)
+  int32_t fp32;           // w and g are float32 (float32 masters: no dither, no cast)
+  int32_t pad3;          // row-band pass: rows per band
   uint64_t tensor_id;
 };
 
@@ -154,7 +156,7 @@ struct TensorPlan {
   int32_t grp0 = 0, ngrp = 1;  // the sub-tensors sharing its clip factor (a stacked tensor's slices)
   int64_t idx0 = 0;            // element index of its first element in the descriptor's tensor
   int64_t n = 0, m = 0, ld = 0, N = 0;
-  int32_t tier = 0, kind = 0, momentum = 0;
+  int32_t tier = 0, kind = 0, momentum = 0, fp32 = 0;
   int64_t tr = 0;
   int32_t cw = 0, ntc = 0, ntr = 0, nfr = 0, nfc = 0;
   bool empty = true;

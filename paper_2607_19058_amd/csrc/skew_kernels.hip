@@ -60,6 +60,10 @@ __device__ __forceinline__ void stg(float4 *p, float4 v) {
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 __device__ __forceinline__ float bf_one(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+// element idx of a weight or gradient array: bf16, or float32 for float32 masters
+__device__ __forceinline__ float elem(const uint16_t *p, int64_t idx, bool fp32) {
+  return fp32 ? ldg(reinterpret_cast<const float *>(p) + idx) : bf_one(ldg(p + idx));
+}
 
 // max(a, b) that returns `a` when it is NaN (b is a finite constant): NaN propagates.
 __device__ __forceinline__ float max_nan(float a, float b) { return (a < b) ? b : a; }
@@ -133,6 +137,16 @@ __device__ __forceinline__ float dither_u16(uint32_t u) { return fmaf((float)u, 
 __device__ __forceinline__ float dither_lo(uint32_t h) { return dither_u16(h & 0xFFFFu); }
 __device__ __forceinline__ float dither_hi(uint32_t h) { return dither_u16(h >> 16); }
 __device__ __forceinline__ float dither_of(uint32_t h, uint64_t idx) { return (idx & 1u) ? dither_hi(h) : dither_lo(h); }
+
+// The noise added before the cast is the product of two exact factors: e 2^-24 and |w|
+// (ulp(w) taken as 2^-7 |w|, Sec. 3), or, in the exact-ulp mode, e 2^-17 and the bf16 ulp
+// of w: 2^(E - 134) for biased exponent E >= 1, 2^-133 among the subnormals
+__device__ __forceinline__ float bf16_ulp(float w) {
+  const uint32_t E = (__float_as_uint(w) >> 23) & 0xFFu;
+  return __uint_as_float(E >= 8u ? (E - 7u) << 23 : 1u << ((E > 0u ? E : 1u) + 15u));
+}
+__device__ __forceinline__ float dither_mul(float w, bool xu) { return xu ? bf16_ulp(w) : fabsf(w); }
+__device__ __forceinline__ float dither_fac(float dith, bool xu) { return xu ? dith * 128.f : dith; }
 
 // fixed-order tree over the work-group (every thread gets the total)
 __device__ __forceinline__ double block_sum(double x, double *sh) {
@@ -1025,7 +1039,7 @@ __global__ __launch_bounds__(kThreads) void gsq_kernel(const DevTensor *__restri
 #pragma unroll
     for (int e = 0; e < 8; e++) {
       if (wm.col + e >= t.m) continue;
-      const double g = (double)bf_one(ldg(t.g + i * t.ld + wm.col + e));
+      const double g = (double)elem(t.g, i * t.ld + wm.col + e, t.fp32);
       acc += g * g;
     }
   }
@@ -1220,7 +1234,7 @@ __device__ __forceinline__ double p2_exact(const DevTensor &t, const Tile &tl, i
     for (int e = 0; e < 8; e++) {
       if (col + e >= m) continue;
       const int64_t sidx = i * m + col + e;
-      float g = bf_one(ldg(t.g + i * ld + col + e));
+      float g = elem(t.g, i * ld + col + e, t.fp32);
       if (k.gclip) g = gc * g;
       const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
       const float dd = sqrtf(max_nan(vn, k.eps));
@@ -1500,11 +1514,11 @@ __device__ __forceinline__ float decayed(float w, bool dec, float wd) { return d
 // D = sqrt(max(R_i * c'_j, eps)), U = ((s * x) / D) * k, y = (wd - lr U) + xi, where wd is
 // the (decayed) starting weight and xi scales with the pre-step |w|.
 __device__ __forceinline__ float exact_factored_y(float x, float w, float wd, float Ri, float cpj, float s,
-                                                  float kc, float eps, float lr, float dith) {
+                                                  float kc, float eps, float lr, float dith, bool xu) {
   const float vh = __fmul_rn(Ri, cpj);
   const float dd = sqrtf(max_nan(vh, eps));
   const float U = __fmul_rn(__fmul_rn(s, x) / dd, kc);
-  return fmaf(dith, fabsf(w), fmaf(-lr, U, wd));
+  return fmaf(dither_fac(dith, xu), dither_mul(w, xu), fmaf(-lr, U, wd));
 }
 
 // y may round differently from the oracle's value when this is >= 0: the fast update x*F
@@ -1557,11 +1571,12 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
     dith[2 * e2 + 1] = dither_hi(h);
   }
   const bool dec = t.decay && k.wd != 0.f;
+  const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
   float slack = -1.f;
 #pragma unroll
   for (int e = 0; e < 8; e++) {
     const float F = fminf(alpha * bf[e], c.cap3);
-    y[e] = fmaf(dith[e], fabsf(w[e]), fmaf(-x[e], F, decayed(w[e], dec, k.wd)));
+    y[e] = fmaf(dither_fac(dith[e], xu), dither_mul(w[e], xu), fmaf(-x[e], F, decayed(w[e], dec, k.wd)));
     slack = fmaxf(slack, boundary_slack(y[e], x[e] * F, w[e]));
   }
   if (slack >= 0.f) {
@@ -1571,7 +1586,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
       const float F = fminf(alpha * bf[e], c.cap3);
       if (near_boundary(y[e], x[e] * F, w[e]))
         y[e] = exact_factored_y(x[e], w[e], decayed(w[e], dec, k.wd), Ri, ldg(t.C + col + e) / c.q, c.s, c.kc,
-                                c.eps, c.lr, dith[e]);
+                                c.eps, c.lr, dith[e], xu);
     }
   }
   stg(reinterpret_cast<uint4 *>(t.w + i * t.ld + col),
@@ -1632,9 +1647,10 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         const float dith = dither_of(dz.pair(idx >> 1), idx);
         const float F = fminf(alpha * (float)col_factor(t, col + e, c.q), c.cap3);
         const float wd = decayed(w, t.decay && k.wd != 0.f, k.wd);
-        float y = fmaf(dith, fabsf(w), fmaf(-x, F, wd));
+        const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
+        float y = fmaf(dither_fac(dith, xu), dither_mul(w, xu), fmaf(-x, F, wd));
         if (near_boundary(y, x * F, w))
-          y = exact_factored_y(x, w, wd, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith);
+          y = exact_factored_y(x, w, wd, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith, xu);
         stg(t.w + i * ld + col + e, to_bf16(y));
       }
     }
@@ -1654,9 +1670,9 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
     for (int e = 0; e < 8; e++) {
       if (col + e >= m) continue;
       const int64_t sidx = i * m + col + e;
-      float g = bf_one(ldg(t.g + i * ld + col + e));
+      float g = elem(t.g, i * ld + col + e, t.fp32);
       if (k.gclip) g = gc * g;
-      const float w = bf_one(ldg(t.w + i * ld + col + e));
+      const float w = elem(t.w, i * ld + col + e, t.fp32);
       const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
       stg(t.V + sidx, vn);
       const float dd = sqrtf(max_nan(vn, k.eps));
@@ -1670,8 +1686,13 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
       }
       const float U = __fmul_rn(num / dd, kc);
       const float x = fmaf(-k.lr, U, decayed(w, t.decay && k.wd != 0.f, k.wd));
+      if (t.fp32) {   // float32 master: no dither, no cast
+        stg(reinterpret_cast<float *>(t.w) + i * ld + col + e, x);
+        continue;
+      }
       const uint64_t idx = (uint64_t)(t.idx0 + sidx);
-      const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), fabsf(w), x);
+      const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
+      const float y = fmaf(dither_fac(dither_of(dz.pair(idx >> 1), idx), xu), dither_mul(w, xu), x);
       stg(t.w + i * ld + col + e, to_bf16(y));
     }
   }

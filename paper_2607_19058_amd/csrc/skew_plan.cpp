@@ -25,7 +25,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     const skew_tensor_desc &x = d[i];
     if (x.tier < SKEW_TIER_BACKBONE || x.tier > SKEW_TIER_ROUTER) return SKEW_EINVAL;
     if (x.ndim < 1 || x.ndim > 3) return SKEW_EINVAL;
-    if ((x.state_flags & ~(uint32_t)(SKEW_STATE_MOMENTUM | SKEW_STATE_FACTORED)) != 0) return SKEW_EINVAL;
+    if ((x.state_flags & ~(uint32_t)(SKEW_STATE_MOMENTUM | SKEW_STATE_FACTORED | SKEW_STATE_FP32)) != 0)
+      return SKEW_EINVAL;
     if (x.ndim == 3 ? x.batch < 0 : (x.batch != 0 && x.batch != 1)) return SKEW_EINVAL;
     const int64_t E = (x.ndim == 3 && x.batch > 1) ? x.batch : 1;
     if (E > INT32_MAX / 4) return SKEW_EINVAL;
@@ -72,6 +73,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     const bool factor_router = (x.state_flags & SKEW_STATE_FACTORED) != 0;
     tp.kind = ((x.tier == SKEW_TIER_ROUTER && !factor_router) || x.ndim == 1) ? kExact : kFactored;
     tp.momentum = (x.tier == SKEW_TIER_BACKBONE || (x.state_flags & SKEW_STATE_MOMENTUM) != 0) ? 1 : 0;
+    tp.fp32 = (x.state_flags & SKEW_STATE_FP32) != 0 ? 1 : 0;
+    if (tp.fp32 && tp.kind != kExact) return SKEW_EINVAL;   // float32 masters: exact-moment tensors
     if (tp.empty) continue;
 
     // state slices: one contiguous array per descriptor (slice e at e times the slice)

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libskewadam.so")
 SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
 FLAG_EXACT_CLIP = 1
-STATE_MOMENTUM, STATE_FACTORED = 1, 2   # tier variants (SKEW_STATE_*)
+STATE_MOMENTUM, STATE_FACTORED, STATE_FP32 = 1, 2, 4   # tier variants (SKEW_STATE_*)
+FLAG_EXACT_ULP = 2
 TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
 ABI_VERSION = 3
 
@@ -118,8 +119,9 @@ def state_bytes(descs: Sequence[TensorDesc]):
 
 def _desc_for(tier: int, w, g, tensor_id: int, state_flags: int = 0) -> TensorDesc:
     import torch
-    if w.dtype != torch.bfloat16 or g.dtype != torch.bfloat16:
-        raise TypeError("weights and gradients must be bfloat16")
+    want = torch.float32 if state_flags & STATE_FP32 else torch.bfloat16
+    if w.dtype != want or g.dtype != want:
+        raise TypeError(f"weights and gradients must be {want} for these state flags")
     if w.device.type != "cuda" or g.device != w.device:
         raise TypeError("weights and gradients must live on the same HIP device")
     if w.shape != g.shape or w.stride() != g.stride():

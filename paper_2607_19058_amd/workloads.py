@@ -37,6 +37,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
+STATE_FP32 = 4   # the tier-variant flag of float32 master weights and gradients
 SIGMA_G, SIGMA_W = 1e-3, 0.02
 
 
@@ -210,7 +211,7 @@ def init_weight(spec: Spec, wl: Workload, device, out=None):
     gen.manual_seed(_seed(wl.seed, 1, spec.tensor_id))
     w = torch.randn(spec.shape, generator=gen, device=device, dtype=torch.float32).mul_(SIGMA_W)
     if out is None:
-        return w.to(torch.bfloat16)
+        return w if spec.state_flags & STATE_FP32 else w.to(torch.bfloat16)   # float32 masters stay float32
     out.copy_(w)
     return out
 

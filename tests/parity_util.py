@@ -76,7 +76,8 @@ class ParityRun:
         self.hp = dict(oracle.DEFAULTS) if hp is None else dict(hp)
         self.specs = specs if specs is not None else wl.specs
         self.W = [W.init_weight(s, wl, self.device) for s in self.specs]
-        self.G = [torch.zeros(s.shape, dtype=torch.bfloat16, device=self.device) for s in self.specs]
+        self.G = [torch.zeros(s.shape, dtype=torch.float32 if s.state_flags & oracle.STATE_FP32 else torch.bfloat16,
+                              device=self.device) for s in self.specs]
         self.opt = SkewAdam([(s.tier, self.W[k], self.G[k], s.tensor_id, s.state_flags)
                              for k, s in enumerate(self.specs)])
         idx = list(range(len(self.specs))) if sample is None else list(sample)
@@ -85,7 +86,7 @@ class ParityRun:
         self.diverged = {}
         for k in idx:
             s = self.specs[k]
-            w = bits(self.W[k])
+            w = self._host(self.W[k])
             self.O[k] = oracle.Tensor(tier=s.tier, w=w.copy(), g=np.zeros_like(w), tensor_id=s.tensor_id,
                                       state_flags=s.state_flags).init_state()
             self.diverged[k] = np.zeros(w.shape, bool)
@@ -96,7 +97,7 @@ class ParityRun:
         for k, s in enumerate(self.specs):
             W.fill_grad(s, self.wl, t, self.G[k], scales)
         for k in self.sample:
-            self.O[k].g = bits(self.G[k])
+            self.O[k].g = self._host(self.G[k])
         torch.cuda.synchronize()
         t0 = time.time()
         # the gradient-norm scaling couples every tensor: an oracle step over a sample gets the
@@ -107,6 +108,8 @@ class ParityRun:
         self.opt.step(t, seed=self.seed, flags=self.flags, **self.hp)
         torch.cuda.synchronize()
         t1 = time.time()
+        if self.flags & 2:   # the exact-ulp dither
+            extra["exact_ulp"] = True
         oracle.step([self.O[k] for k in self.sample], t, seed=self.seed, want_y=True, **self.hp, **extra)
         t2 = time.time()
         st = Stats()
@@ -122,6 +125,11 @@ class ParityRun:
             self.stats.state_bad[key] = self.stats.state_bad.get(key, 0) + v
         log(f"  step {t}: gpu {1e3 * (t1 - t0):.1f} ms, oracle {t2 - t1:.2f} s; {st}")
         return st
+
+    @staticmethod
+    def _host(t: torch.Tensor) -> np.ndarray:
+        """bf16 bits (uint16), or float32 values for float32 masters."""
+        return t.detach().cpu().numpy().copy() if t.dtype == torch.float32 else bits(t)
 
     def _compare(self, k: int, st: Stats):
         o, s = self.O[k], self.specs[k]
@@ -151,6 +159,14 @@ class ParityRun:
                 st.max_rel_rc = max(st.max_rel_rc, float(np.nanmax(rel)))
             if bad:
                 st.state_bad[f"{s.name}.{name}"] = bad
+        if o.w.dtype == np.float32:
+            # float32 masters: the oracle's own float sequence, bit for bit
+            gwf = self.W[k].detach().cpu().numpy().reshape(o.w.shape)
+            bad = int(np.count_nonzero(gwf.view(np.uint32) != o.w.view(np.uint32)))
+            st.compared += o.w.size
+            if bad:
+                st.state_bad[f"{s.name}.w32"] = bad
+            return
         gw = bits(self.W[k]).reshape(o.w.shape)
         ow = o.w
         mism = gw != ow

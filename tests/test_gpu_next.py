@@ -217,3 +217,40 @@ def test_stacked_more_than_2p31_elements():
     st = run(wl)
     assert st.ok(), st
     assert st.compared >= 2 * 129 * 4096 * 4096
+
+
+# ----------------------------------------------------------------------------- exact ulp, fp32 masters
+def test_exact_ulp_dither_tiny_every_tensor():
+    from paper_2607_19058_amd.skewadam import FLAG_EXACT_ULP
+    log("[parity] tiny with the exact-ulp dither, 10 steps, all compared")
+    st = run(W.get("tiny"), flags=FLAG_EXACT_ULP)
+    assert st.ok(), st
+
+
+def test_exact_ulp_dither_unit_shapes_with_decay():
+    from paper_2607_19058_amd.skewadam import FLAG_EXACT_ULP
+    log("[parity] unit shapes, exact-ulp dither and strong decay, 3 steps")
+    st = run(_unit_workload(), hp=dict(oracle.DEFAULTS, lr=1e-2, weight_decay=2.0), flags=FLAG_EXACT_ULP)
+    assert st.ok(), st
+
+
+def test_fp32_masters_router_and_norms():
+    """Float32 master weights for the router and the vectors (the paper's fp32 router and
+    norms, Table 5): updated in float32 with no cast, bit for bit with the oracle, beside
+    bf16 tensors, with decay and the gradient-norm scaling."""
+    import dataclasses
+    base = _unit_workload()
+    specs = [dataclasses.replace(s, state_flags=oracle.STATE_FP32)
+             if (s.tier == W.ROUTER or len(s.shape) == 1) else s for s in base.specs]
+    wl = W.Workload("unit_fp32", specs, 3)
+    log("[parity] unit shapes with float32 router and vectors, decay and gradient norm, 3 steps")
+    st = run(wl, hp=dict(oracle.DEFAULTS, lr=1e-2, weight_decay=0.5, max_grad_norm=0.05))
+    assert st.ok(), st
+
+
+def test_fp32_master_refused_on_factored_tensors():
+    dev = torch.device("cuda")
+    w = torch.zeros((4, 8), dtype=torch.float32, device=dev)
+    from paper_2607_19058_amd import SkewError
+    with pytest.raises(SkewError):
+        SkewAdam([(W.EXPERT, w, w.clone(), 0, oracle.STATE_FP32)])

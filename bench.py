@@ -56,8 +56,23 @@ def tier_class(spec) -> str:
     return "backbone_vector" if vec else "backbone_matrix"
 
 
+def bytes_per_param(spec) -> int:
+    """G read (2) + W read and written (4) + fp32 momentum read and written (8) where the
+    tier or its variant keeps one + the exact second moment read and written (8)."""
+    from paper_2607_19058_amd import workloads as W
+    flags = getattr(spec, "state_flags", 0)
+    vec = len(spec.shape) == 1
+    momentum = spec.tier == W.BACKBONE or bool(flags & 1)
+    exact = vec or (spec.tier == W.ROUTER and not flags & 2)
+    wbytes = 12 if flags & 4 else 6    # float32 master: G 4 + W 8
+    return wbytes + (8 if momentum else 0) + (8 if exact else 0)
+
+
 def algorithmic_bytes(specs) -> int:
-    return sum(BYTES_PER_PARAM[tier_class(s)] * s.numel for s in specs)
+    total = sum(bytes_per_param(s) * s.numel for s in specs)
+    assert all(bytes_per_param(s) == BYTES_PER_PARAM[tier_class(s)] for s in specs
+               if not getattr(s, "state_flags", 0))
+    return total
 
 
 def kernel_sha() -> str:
@@ -112,6 +127,12 @@ def main() -> int:
     ap.add_argument("--max-grad-norm", type=float, default=0.0,
                     help="> 0: the step scales the gradients by the global-norm factor (two-pass "
                          "statistics); the bench also times torch's unfused clip_grad_norm_ on the same G")
+    ap.add_argument("--variant", default="skewadam", choices=["skewadam", "expert_momentum", "factored_router",
+                                                              "uniform"],
+                    help="tier variant of the ablation (state flags per tier)")
+    ap.add_argument("--stacked", action="store_true",
+                    help="each expert projection as one stacked (E, n, m) tensor")
+    ap.add_argument("--exact-ulp", action="store_true", help="dither of one exact bf16 ulp")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three plain 1 GiB device-to-device copies (read 1 GiB, write 1 GiB "
                          "each), whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures")
@@ -141,10 +162,13 @@ def main() -> int:
         del src, dst
         log("[bench] calibration copies done (3 x 1 GiB)")
     wl = W.get(args.workload)
+    if args.stacked:
+        wl = W.stacked(wl)
+    wl = W.with_variant(wl, args.variant)
     log(f"[bench] workload {wl.name}: {len(wl.specs)} tensors, {wl.numel:,} params; allocating")
     Wt = [W.init_weight(s, wl, dev) for s in wl.specs]
     G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
-    opt = SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id) for k, s in enumerate(wl.specs)])
+    opt = SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id, s.state_flags) for k, s in enumerate(wl.specs)])
 
     def draw(t):
         sc = W.expert_scales(wl, t)
@@ -152,7 +176,8 @@ def main() -> int:
             W.fill_grad(s, wl, t, G[k], sc)
 
     hp = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0, seed=0,
-              weight_decay=args.weight_decay, max_grad_norm=args.max_grad_norm)
+              weight_decay=args.weight_decay, max_grad_norm=args.max_grad_norm,
+              flags=2 if args.exact_ulp else 0)
     for t in range(1, args.warmup + 1):
         draw(t)
         opt.step(t, **hp)
@@ -232,7 +257,8 @@ def main() -> int:
                                "(bf16 weights and gradients, fp32 state)",
                    "params": params, "tensors": len(wl.specs), "state_bytes": opt.state_nbytes,
                    "workspace_bytes": opt.workspace_nbytes, "weight_decay": args.weight_decay,
-                   "max_grad_norm": args.max_grad_norm},
+                   "max_grad_norm": args.max_grad_norm, "variant": args.variant, "stacked": args.stacked,
+                   "exact_ulp": args.exact_ulp},
         "roofline": roof,
         "step": {"algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3),
                  "effective_GBps": round(step_gbps, 1), "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),

@@ -156,6 +156,48 @@ def ragged() -> Workload:
     return Workload("ragged", specs, 50, banks={0: 64, 1: 64}, zero_per_step={0: 3, 1: 3})
 
 
+def stacked(wl: Workload) -> Workload:
+    """The same parameters with each expert projection of a bank stacked into one
+    (E, n, m) tensor (slice e = expert e), in place of E separate matrices."""
+    import dataclasses
+    groups: Dict[tuple, List[Spec]] = {}
+    order: List[object] = []
+    for s in wl.specs:
+        if s.tier == EXPERT and s.bank >= 0 and len(s.shape) == 2:
+            key = (s.bank, s.name.split(".", 1)[-1], s.shape)
+            if key not in groups:
+                groups[key] = []
+                order.append(key)
+            groups[key].append(s)
+        else:
+            order.append(s)
+    specs: List[Spec] = []
+    for item in order:
+        if isinstance(item, Spec):
+            specs.append(dataclasses.replace(item, tensor_id=len(specs)))
+            continue
+        members = sorted(groups[item], key=lambda x: x.expert)
+        bank, proj, shape = item
+        assert [m.expert for m in members] == list(range(len(members))), "experts 0..E-1 of the bank"
+        specs.append(Spec(f"ex.{proj}", EXPERT, (len(members),) + shape, len(specs), bank=bank, expert=0))
+    return dataclasses.replace(wl, name=wl.name + "_stacked", specs=specs)
+
+
+VARIANTS = {   # tier variants of the ablation (Table 3): state flags by tier
+    "skewadam": {},
+    "expert_momentum": {EXPERT: 1},
+    "factored_router": {ROUTER: 2},
+    "uniform": {BACKBONE: 3, EXPERT: 3, ROUTER: 3},
+}
+
+
+def with_variant(wl: Workload, variant: str) -> Workload:
+    import dataclasses
+    flags = VARIANTS[variant]
+    specs = [dataclasses.replace(s, state_flags=flags.get(s.tier, 0)) for s in wl.specs]
+    return dataclasses.replace(wl, name=f"{wl.name}_{variant}" if flags else wl.name, specs=specs)
+
+
 def tiny_stacked() -> Workload:
     """The tiny workload with each expert bank projection stacked into one (8, n, m) tensor."""
     base = tiny()

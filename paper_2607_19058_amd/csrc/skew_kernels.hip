@@ -916,6 +916,37 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
     p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
 }
 
+// Reductions of the clip stage, over the whole work-group (a tensor of its own) or over one
+// wave (the slices of a stacked tensor, one slice per wave at a time). Every participating
+// lane gets the result, in a fixed order.
+struct RedGroup {
+  double *sh;
+  static constexpr int kN = kThreads;
+  __device__ __forceinline__ int lane() const { return (int)threadIdx.x; }
+  __device__ __forceinline__ bool lead() const { return threadIdx.x == 0; }
+  __device__ __forceinline__ double sum(double x) const { return block_sum(x, sh); }
+  __device__ __forceinline__ double max(double x) const { return wg_max_w<kWaves>(x, sh); }
+  __device__ __forceinline__ float minf(float x) const { return wg_min_wf<kWaves>(x, sh); }
+  __device__ __forceinline__ float maxf(float x) const { return wg_max_wf<kWaves>(x, sh); }
+  __device__ __forceinline__ int any(int x) const { return wg_or_w<kWaves>(x, sh); }
+};
+struct RedWave {
+  static constexpr int kN = 64;
+  __device__ __forceinline__ int lane() const { return (int)(threadIdx.x & 63); }
+  __device__ __forceinline__ bool lead() const { return (threadIdx.x & 63) == 0; }
+  __device__ __forceinline__ double sum(double x) const { return wave_sum_d(x); }
+  __device__ __forceinline__ double max(double x) const { return wave_max_d(x); }
+  __device__ __forceinline__ float minf(float x) const { return wave_min_f(x); }
+  __device__ __forceinline__ float maxf(float x) const { return wave_max_f(x); }
+  __device__ __forceinline__ int any(int x) const { return wave_or(x); }
+};
+template <class Red>
+__device__ __forceinline__ double red_sum(const Red &r, const double *p, int64_t n, int64_t stride = 1) {
+  double s = 0.0;
+  for (int64_t c = r.lane(); c < n; c += Red::kN) s += ldg(p + c * stride);
+  return r.sum(s);
+}
+
 // fixed-order work-group sum of p[0], p[stride], ..., p[(n-1) stride]: thread j sums
 // entries j, j + 256, ..., then a tree; every thread of the (256-thread) work-group calls it
 __device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh, int64_t stride = 1) {
@@ -925,12 +956,16 @@ __device__ __forceinline__ double wg_sum(const double *p, int64_t n, double *sh,
 }
 // q = max(mean R, eps) for a factored tensor (the clamp of the reconstruction), from the
 // sums of R over the fold chunks of rows or over the row bands
-__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, const StepConsts &k, double *sh) {
+template <class Red>
+__device__ __forceinline__ float mean_r_of(const DevTensor &t, const StepConsts &k, const Red &r) {
   // row-band tensors keep the sums of R in their band statistics, except in the gradient-
   // norm mode, where the fold forms R and its sums per chunk of rows as for wide tensors
-  const double sr = (t.zpath && !k.gclip) ? wg_sum(&t.bst->rsum, t.nzb, sh, sizeof(BandStats) / sizeof(double))
-                                          : wg_sum(t.rsum, t.zpath ? (t.n + kFold - 1) / kFold : t.nfr, sh);
+  const double sr = (t.zpath && !k.gclip) ? red_sum(r, &t.bst->rsum, t.nzb, sizeof(BandStats) / sizeof(double))
+                                          : red_sum(r, t.rsum, t.zpath ? (t.n + kFold - 1) / kFold : t.nfr);
   return max_nan((float)(sr / (double)t.n), k.eps);
+}
+__device__ __forceinline__ float mean_r_clamped(const DevTensor &t, const StepConsts &k, double *sh) {
+  return mean_r_of(t, k, RedGroup{sh});
 }
 
 // --------------------------------------------------------------------------------------------
@@ -1339,167 +1374,247 @@ __device__ __forceinline__ float clip_from_sum(double S, double N, float d, doub
 }
 
 // clip factors of the listed tensors from the re-check's sums; level 1 lists for level 2
-// the tensors whose spread still leaves k undecided
+// the tensors whose spread still leaves k undecided. A stacked tensor's slices are listed
+// together; the work-group of its first slice decides k for all of them (one slice per
+// wave at a time), the others return.
 __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor *__restrict__ TT, RecheckLists *L,
                                                                 int ntensors, StepConsts k, int level) {
   __shared__ double sh[kThreads];
+  __shared__ double wsum[kWaves][3];
+  __shared__ float kf_sh;
+  __shared__ int amb_sh, pos_sh;
   const int n = ldg(level == 1 ? &L->n1 : &L->n2);
   if ((int)blockIdx.x >= n) return;
   const int ti = ldg(recheck_list(L, ntensors, level) + blockIdx.x);
   const DevTensor &t0 = TT[ti];
-  // a group's slices are listed together; its first slice decides k for all of them
   if (t0.grp0 != ti) return;
   const int ng = t0.ngrp;
   double S = 0.0, Q4 = 0.0, N = 0.0;
-  for (int e = 0; e < ng; e++) {
-    const DevTensor &t = TT[ti + e];
-    const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
-    S += wg_sum(t.ssum, ntiles, sh);
-    if (level == 1) Q4 += wg_sum(t.qsum, ntiles, sh);
-    N += (double)(t.n * t.m);
+  if (ng == 1) {
+    const int64_t ntiles = (int64_t)t0.ntr * t0.ntc * kSub;   // per-part sums
+    S = red_sum(RedGroup{sh}, t0.ssum, ntiles);
+    if (level == 1) Q4 = red_sum(RedGroup{sh}, t0.qsum, ntiles);
+    N = (double)(t0.n * t0.m);
+  } else {
+    const int w = (int)(threadIdx.x >> 6);
+    double s = 0.0, q4 = 0.0, nn = 0.0;
+    for (int e = w; e < ng; e += kWaves) {
+      const DevTensor &t = TT[ti + e];
+      const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;
+      s += red_sum(RedWave{}, t.ssum, ntiles);
+      if (level == 1) q4 += red_sum(RedWave{}, t.qsum, ntiles);
+      nn += (double)(t.n * t.m);
+    }
+    if ((threadIdx.x & 63) == 0) {
+      wsum[w][0] = s;
+      wsum[w][1] = q4;
+      wsum[w][2] = nn;
+    }
+    __syncthreads();
+    for (int v = 0; v < kWaves; v++) {   // waves in order
+      S += wsum[v][0];
+      Q4 += wsum[v][1];
+      N += wsum[v][2];
+    }
   }
-  if (threadIdx.x != 0) return;
-  bool amb = false;
-  const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
-  const float kf = clip_from_sum(S, N, k.d, spread, amb);
+  if (threadIdx.x == 0) {
+    bool amb = false;
+    const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
+    kf_sh = clip_from_sum(S, N, k.d, spread, amb);
+    amb_sh = amb;
+    pos_sh = amb ? atomicAdd(&L->n2, ng) : 0;
+  }
+  __syncthreads();
+  const float kf = kf_sh;
+  const bool amb = amb_sh != 0;
+  const int pos = pos_sh;
   const int why = ldg(&t0.sc->ambiguous) & ~0xF;
-  if (amb) {
-    const int pos = atomicAdd(&L->n2, ng);
-    for (int e = 0; e < ng; e++) {
+  for (int e = (int)threadIdx.x; e < ng; e += kThreads) {
+    if (amb) {
       stg(recheck_list(L, ntensors, 2) + pos + e, (int32_t)(ti + e));
       stg(&TT[ti + e].sc->ambiguous, (int32_t)(kClipPending2 | (kWhySpread << 4)));
+    } else {
+      stg(&TT[ti + e].sc->k, kf);
+      stg(&TT[ti + e].sc->ambiguous, (int32_t)(why | (level == 1 ? kClipSplit : kClipExact)));
     }
-    return;
-  }
-  for (int e = 0; e < ng; e++) {
-    stg(&TT[ti + e].sc->k, kf);
-    stg(&TT[ti + e].sc->ambiguous, (int32_t)(why | (level == 1 ? kClipSplit : kClipExact)));
   }
 }
 
-// --------------------------------------------------------------------------------------------
-// clip stage, one work-group per tensor: k = 1 / max(1, RMS(U_hat) / d) (Sec. 3, Alg. 1),
-// NaN-propagating and rounded once to float as the oracle rounds it. With exact == 0 it
-// also records q = max(mean R, eps) and flags the tensor when k's rounding is not decided
-// by the approximate sum: its spread (20 standard deviations of the free roundings)
-// reaches a rounding boundary of k or the clipping threshold. With exact == 1 it
-// recomputes k of flagged tensors from the exact pass's sums.
+// One slice's share of the clip stage (a tensor, or one slice of a stacked tensor): the
+// estimate of its sum of U_hat^2, the estimate's absolute error bound, and whether its
+// floor regime leaves the sum open (the estimate is then an upper bound). Records q and
+// the next step's floor regime of the slice.
 //
 // Row-band tensors: when no element is on the eps floor (min R_i * min c'_j >= eps) the
 // sum is sum_j z_j / c'_j, with a spread bounded through max (s x)^2 / (R_i c'_j); when
 // every element is (max R_i * max c'_j < eps) it is the exactly rounded floored sum.
 // Otherwise both are upper bounds of the oracle's sum (an element's U_hat^2 is at most
-// its unfloored and its floored value, up to rounding); below the clipping threshold k
-// is exactly 1, and above it the tensor goes to the exact pass.
+// its unfloored and its floored value, up to rounding).
+struct SliceSum {
+  double S, E;
+  int open;   // 0, or why the sum is open (kWhyStraddle, kWhyMissingSum)
+  int bad;    // a non-finite sum or statistic
+};
+template <class Red>
+__device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepConsts &k, const Red &r) {
+  SliceSum o = {0.0, 0.0, 0, 0};
+  const float q = t.kind == kFactored ? mean_r_of(t, k, r) : 0.f;
+  if (t.zpath) {
+    const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
+    const double Y = red_sum(r, &t.bst->ysum, t.nzb, bstride);
+    const double SU = red_sum(r, &t.cst->s, t.nfc, cstride);
+    double um = 0.0;
+    float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
+    int bad = 0;
+    for (int64_t b = r.lane(); b < t.nzb; b += Red::kN) {
+      um = fmax(um, ldg(&t.bst[b].umax));
+      rmn = fminf(rmn, ldg(&t.bst[b].rmin));
+      rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
+      bad |= ldg(&t.bst[b].bad);
+    }
+    for (int64_t c = r.lane(); c < t.nfc; c += Red::kN) {
+      cmn = fminf(cmn, ldg(&t.cst[c].cmin));
+      cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
+      bad |= ldg(&t.cst[c].bad);
+    }
+    um = r.max(um);
+    rmn = r.minf(rmn);
+    rmx = r.maxf(rmx);
+    cmn = r.minf(cmn);
+    cmx = r.maxf(cmx);
+    bad = r.any(bad);
+    // the sums the row-band pass formed this step (it skips one when the last step
+    // predicts the regime); a sum it did not form counts as +inf
+    const int formed = ldg(&t.bst[0].regime);
+    const bool have_z = formed != kRegimeFloor, have_y = formed != kRegimeAbove;
+    const double inf = __builtin_inf();
+    const double SUf = have_z ? SU : inf, Yf = have_y ? Y : inf;
+    const bool finite = !(SUf != SUf) && !(Yf != Yf) && (SUf < 1e300 || Yf < 1e300);
+    const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
+    if (bad || !finite) {
+      o.bad = 1;
+      o.S = SU;
+    } else if (have_z && lo >= k.eps) {   // nothing on the floor
+      o.S = SU;
+      o.E = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) + 1e-14 * SU : 0.0;
+    } else if (have_y && hi < k.eps) {    // everything on the floor
+      o.S = Y;
+      o.E = 1e-14 * Y;
+    } else {
+      o.S = fmin(SUf, Yf) * (1.0 + 1e-6);  // an upper bound of the oracle's sum
+      o.open = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
+    }
+    // the next step's prediction, with a factor-2 margin on either side of the floor
+    const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
+    if (r.lead()) stg(&t.sc->regime, o.bad ? (int32_t)kRegimeBoth : (int32_t)next);
+  } else {
+    const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
+    o.S = red_sum(r, t.ssum, ntiles);
+    const double Q4 = red_sum(r, t.qsum, ntiles);
+    // the exact second moment's sum is the oracle's own; a factored one carries the
+    // spread of its unrounded terms (20 standard deviations)
+    o.E = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) + 1e-14 * o.S : 0.0;
+  }
+  if (r.lead()) stg(&t.sc->q, q);
+  return o;
+}
+
+// --------------------------------------------------------------------------------------------
+// clip stage, one work-group per tensor (or per stacked tensor, whose slices share one k):
+// k = 1 / max(1, RMS(U_hat) / d) (Sec. 3, Alg. 1), NaN-propagating and rounded once to
+// float as the oracle rounds it. It records q = max(mean R, eps) and flags the tensor when
+// k's rounding is not decided by the approximate sum: its spread (20 standard deviations
+// of the free roundings) reaches a rounding boundary of k or the clipping threshold. When
+// a slice's floor regime leaves its sum open, the group's sum is an upper bound: below
+// the clipping threshold k is exactly 1, and above it the tensor goes to a re-check.
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restrict__ TT,
                                                         const Item *__restrict__ items, StepConsts k,
                                                         RecheckLists *L, int ntensors) {
   __shared__ double sh[kThreads];
+  __shared__ double wsum[kWaves][3];
+  __shared__ int wflag[kWaves][2];
+  __shared__ float kf_sh;
+  __shared__ int st_sh, pos_sh;
   const Item it = items[blockIdx.x];   // the first sub-tensor of a group sharing one k
   const DevTensor &t0 = TT[it.tensor];
   const int g0 = t0.grp0, ng = t0.ngrp;
   // the group's sum S as the sum of its slices' estimates, with the sum of their absolute
-  // error bounds; a slice whose floor regime leaves its sum open contributes an upper bound
+  // error bounds, in slice order within a wave and then wave by wave
   double S = 0.0, err = 0.0, N = 0.0;
-  bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t0.kind == kFactored;
-  int why = amb ? kWhyForced : 0;
-  bool open = false, bad_any = false;
-  for (int e = 0; e < ng; e++) {
-    const DevTensor &t = TT[g0 + e];
-    N += (double)(t.n * t.m);
-    const float q = t.kind == kFactored ? mean_r_clamped(t, k, sh) : 0.f;
-    double Se = 0.0, Ee = 0.0;   // the slice's estimate and its error bound
-    if (t.zpath) {
-      const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
-      const double Y = wg_sum(&t.bst->ysum, t.nzb, sh, bstride);
-      const double SU = wg_sum(&t.cst->s, t.nfc, sh, cstride);
-      double um = 0.0;
-      float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
-      int bad = 0;
-      for (int64_t b = threadIdx.x; b < t.nzb; b += kThreads) {
-        um = fmax(um, ldg(&t.bst[b].umax));
-        rmn = fminf(rmn, ldg(&t.bst[b].rmin));
-        rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
-        bad |= ldg(&t.bst[b].bad);
-      }
-      for (int64_t c = threadIdx.x; c < t.nfc; c += kThreads) {
-        cmn = fminf(cmn, ldg(&t.cst[c].cmin));
-        cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
-        bad |= ldg(&t.cst[c].bad);
-      }
-      um = wg_max_w<kWaves>(um, sh);
-      rmn = wg_min_wf<kWaves>(rmn, sh);
-      rmx = wg_max_wf<kWaves>(rmx, sh);
-      cmn = wg_min_wf<kWaves>(cmn, sh);
-      cmx = wg_max_wf<kWaves>(cmx, sh);
-      bad = wg_or_w<kWaves>(bad, sh);
-      if (threadIdx.x == 0) {
-        // the sums the row-band pass formed this step (it skips one when the last step
-        // predicts the regime); a sum it did not form counts as +inf
-        const int formed = ldg(&t.bst[0].regime);
-        const bool have_z = formed != kRegimeFloor, have_y = formed != kRegimeAbove;
-        const double inf = __builtin_inf();
-        const double SUf = have_z ? SU : inf, Yf = have_y ? Y : inf;
-        const bool finite = !(SUf != SUf) && !(Yf != Yf) && (SUf < 1e300 || Yf < 1e300);
-        const float lo = __fmul_rn(rmn, cmn), hi = __fmul_rn(rmx, cmx);
-        if (bad || !finite) {
-          bad_any = true;
-          Se = SU;
-        } else if (have_z && lo >= k.eps) {   // nothing on the floor
-          Se = SU;
-          Ee = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) + 1e-14 * SU : 0.0;
-        } else if (have_y && hi < k.eps) {    // everything on the floor
-          Se = Y;
-          Ee = 1e-14 * Y;
-        } else {
-          Se = fmin(SUf, Yf) * (1.0 + 1e-6);  // an upper bound of the oracle's sum
-          if (!open && !amb) why = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
-          open = true;
-        }
-        // the next step's prediction, with a factor-2 margin on either side of the floor
-        const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
-        stg(&t.sc->regime, (bad || !finite) ? (int32_t)kRegimeBoth : (int32_t)next);
+  int open = 0;   // why the first open slice (in slice order) is open
+  bool bad_any = false;
+  if (ng == 1) {
+    const SliceSum o = slice_sum(t0, k, RedGroup{sh});
+    S = o.S;
+    err = o.E;
+    N = (double)(t0.n * t0.m);
+    open = o.open;
+    bad_any = o.bad != 0;
+  } else {
+    const int w = (int)(threadIdx.x >> 6);
+    double s = 0.0, e_ = 0.0, nn = 0.0;
+    int first = 0x7fffffff, bad = 0;   // 8 x (the first open slice) + why
+    for (int e = w; e < ng; e += kWaves) {
+      const DevTensor &t = TT[g0 + e];
+      const SliceSum o = slice_sum(t, k, RedWave{});
+      s += o.S;
+      e_ += o.E;
+      nn += (double)(t.n * t.m);
+      if (o.open && first == 0x7fffffff) first = 8 * e + o.open;
+      bad |= o.bad;
+    }
+    if ((threadIdx.x & 63) == 0) {
+      wsum[w][0] = s;
+      wsum[w][1] = e_;
+      wsum[w][2] = nn;
+      wflag[w][0] = first;
+      wflag[w][1] = bad;
+    }
+    __syncthreads();
+    int f = 0x7fffffff;
+    for (int v = 0; v < kWaves; v++) {   // waves in order
+      S += wsum[v][0];
+      err += wsum[v][1];
+      N += wsum[v][2];
+      f = min(f, wflag[v][0]);
+      bad_any |= wflag[v][1] != 0;
+    }
+    open = f == 0x7fffffff ? 0 : (f & 7);
+  }
+  if (threadIdx.x == 0) {
+    bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t0.kind == kFactored;
+    int why = amb ? kWhyForced : (open ? open : 0);
+    int level = 2;   // the re-check a flagged group gets
+    double spread = 0.0;
+    if (bad_any) {
+      amb = true;
+      why = kWhyNonFinite;
+    } else if (open) {
+      S += err;   // an upper bound of the group's sum
+      if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
+        amb = true;
+        level = 1;   // the floor split per element decides most of these
       }
     } else {
-      const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
-      Se = wg_sum(t.ssum, ntiles, sh);
-      const double Q4 = wg_sum(t.qsum, ntiles, sh);
-      // the exact second moment's sum is the oracle's own; a factored one carries the
-      // spread of its unrounded terms (20 standard deviations)
-      Ee = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) + 1e-14 * Se : 0.0;
+      spread = S > 0.0 ? err / S : 0.0;
     }
-    if (threadIdx.x == 0) {
-      S += Se;
-      err += Ee;
-      stg(&t.sc->q, q);
-    }
+    const bool flagged_before = amb;
+    kf_sh = clip_from_sum(S, N, k.d, spread, amb);
+    if (amb && !flagged_before) why = kWhySpread;
+    const bool list = amb && t0.kind == kFactored;
+    pos_sh = list ? atomicAdd(level == 1 ? &L->n1 : &L->n2, ng) : 0;
+    st_sh = list ? (int)((level == 1 ? kClipPending1 : kClipPending2) | (why << 4)) | (level << 16) : -1;
   }
-  if (threadIdx.x != 0) return;
-  int level = 2;   // the re-check a flagged group gets
-  double spread = 0.0;
-  if (bad_any) {
-    amb = true;
-    why = kWhyNonFinite;
-  } else if (open) {
-    S += err;   // an upper bound of the group's sum
-    if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
-      amb = true;
-      level = 1;   // the floor split per element decides most of these
-    }
-  } else {
-    spread = S > 0.0 ? err / S : 0.0;
-  }
-  const bool flagged_before = amb;
-  const float kf = clip_from_sum(S, N, k.d, spread, amb);
-  if (amb && !flagged_before) why = kWhySpread;
-  const int pos = (amb && t0.kind == kFactored) ? atomicAdd(level == 1 ? &L->n1 : &L->n2, ng) : 0;
-  for (int e = 0; e < ng; e++) {
+  __syncthreads();
+  const float kf = kf_sh;
+  const int st = st_sh, pos = pos_sh;
+  for (int e = (int)threadIdx.x; e < ng; e += kThreads) {
     const DevTensor &t = TT[g0 + e];
     stg(&t.sc->k, kf);
-    if (amb && t0.kind == kFactored) {
-      stg(recheck_list(L, ntensors, level) + pos + e, (int32_t)(g0 + e));
-      stg(&t.sc->ambiguous, (int32_t)((level == 1 ? kClipPending1 : kClipPending2) | (why << 4)));
+    if (st >= 0) {
+      stg(recheck_list(L, ntensors, st >> 16) + pos + e, (int32_t)(g0 + e));
+      stg(&t.sc->ambiguous, (int32_t)(st & 0xFFFF));
     } else {
       stg(&t.sc->ambiguous, (int32_t)kClipFast);
     }

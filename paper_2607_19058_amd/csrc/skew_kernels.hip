@@ -892,9 +892,10 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   }
 }
 
-template <int NSEG, bool MOM, bool VEC>
+// GN: the gradient-norm mode's passes (mode 1 or 2); without it the mode is 0 at compile time
+template <int NSEG, bool MOM, bool VEC, bool GN>
 __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restrict__ TT,
-                                                        const Item *__restrict__ items, StepConsts k, int mode) {
+                                                        const Item *__restrict__ items, StepConsts k, int mode_arg) {
   __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes];
   __shared__ __attribute__((aligned(16))) unsigned char bufB[kZLdsBytes];
   __shared__ float rbA[64], rbB[64];
@@ -904,6 +905,7 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   __shared__ __attribute__((aligned(16))) unsigned char zlds[2048];   // zeros: 32 bytes per lane
   reinterpret_cast<uint32_t *>(zlds)[threadIdx.x] = 0u;   // complete before the first block's wait
   static_assert(kZThreads * 4 == 2048, "one word per thread");
+  const int mode = GN ? mode_arg : 0;
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
@@ -1655,6 +1657,7 @@ struct P3Scalars {
 // one row segment of 8 elements (vector path): momentum, update, dither, bf16 store.
 // The fast path forms 1/D from per-row and per-column factors; the few elements whose
 // result might round to the other bf16 neighbour take the oracle's exact sequence.
+template <bool XU, bool DEC, bool GC>
 __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k, const P3Scalars &c,
                                         const Dither &dz, int64_t i, int64_t col, const float *bf, uint4 gw,
                                         uint4 ww, const float *mv) {
@@ -1662,7 +1665,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
   float x[8], w[8];
   unpack8(gw, x);
   unpack8(ww, w);
-  if (k.gclip) {
+  if (GC) {
 #pragma unroll
     for (int e = 0; e < 8; e++) x[e] = c.gc * x[e];
   }
@@ -1685,8 +1688,8 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
     dith[2 * e2] = dither_lo(h);
     dith[2 * e2 + 1] = dither_hi(h);
   }
-  const bool dec = t.decay && k.wd != 0.f;
-  const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
+  const bool dec = DEC && t.decay;
+  constexpr bool xu = XU;
   float slack = -1.f;
 #pragma unroll
   for (int e = 0; e < 8; e++) {
@@ -1709,6 +1712,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
                  pack_bf16x2(y[6], y[7])));
 }
 
+template <bool XU, bool DEC, bool GC>
 __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, const StepConsts &k, float kc,
                                             float q, const Dither &dz) {
   const WaveMap wm(t, tl);
@@ -1722,7 +1726,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
   c.eps = k.eps;
   c.lr = k.lr;
   c.lsk = (double)k.lr * (double)c.s * (double)kc;   // lr * s * k
-  c.gc = k.gclip ? ldg(k.gscale) : 1.f;             // gradient-norm mode: elements are fl(c g)
+  c.gc = GC ? ldg(k.gscale) : 1.f;             // gradient-norm mode: elements are fl(c g)
   c.cap3 = (float)(c.lsk / (double)sqrtf(k.eps));
   if (t.vec) {
     float bf[8];
@@ -1740,8 +1744,8 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         load_m8(t.M + i * m + col, ma);
         load_m8(t.M + i2 * m + col, mb);
       }
-      p3_row8(t, k, c, dz, i, col, bf, ga, wa, ma);
-      if (two) p3_row8(t, k, c, dz, i2, col, bf, gb, wb, mb);
+      p3_row8<XU, DEC, GC>(t, k, c, dz, i, col, bf, ga, wa, ma);
+      if (two) p3_row8<XU, DEC, GC>(t, k, c, dz, i2, col, bf, gb, wb, mb);
     }
   } else {
     for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
@@ -1753,7 +1757,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         if (col + e >= m) continue;
         float x = bf_one(ldg(t.g + i * ld + col + e));
         const float w = bf_one(ldg(t.w + i * ld + col + e));
-        if (k.gclip) x = c.gc * x;
+        if (GC) x = c.gc * x;
         if (mom) {
           x = fmaf(k.a1, x, __fmul_rn(k.b1, ldg(t.M + i * m + col + e)));
           stg(t.M + i * m + col + e, x);
@@ -1761,8 +1765,8 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         const uint64_t idx = rowidx + (uint64_t)(col + e);
         const float dith = dither_of(dz.pair(idx >> 1), idx);
         const float F = fminf(alpha * (float)col_factor(t, col + e, c.q), c.cap3);
-        const float wd = decayed(w, t.decay && k.wd != 0.f, k.wd);
-        const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
+        const float wd = decayed(w, DEC && t.decay, k.wd);
+        constexpr bool xu = XU;
         float y = fmaf(dither_fac(dith, xu), dither_mul(w, xu), fmaf(-x, F, wd));
         if (near_boundary(y, x * F, w))
           y = exact_factored_y(x, w, wd, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith, xu);
@@ -1772,13 +1776,14 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
   }
 }
 
+template <bool XU, bool DEC, bool GC>
 __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, const StepConsts &k, float kc,
                                          const Dither &dz) {
   // exact second moment: the oracle's operation order exactly
   const WaveMap wm(t, tl);
   const int64_t m = t.m, ld = t.ld, col = wm.col;
   const bool mom = t.momentum != 0;
-  const float gc = k.gclip ? ldg(k.gscale) : 1.f;
+  const float gc = GC ? ldg(k.gscale) : 1.f;
   for (int64_t lr = wm.wr; lr < tl.nr; lr += wm.rpi) {
     const int64_t i = tl.row(lr);
 #pragma unroll
@@ -1786,7 +1791,7 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
       if (col + e >= m) continue;
       const int64_t sidx = i * m + col + e;
       float g = elem(t.g, i * ld + col + e, t.fp32);
-      if (k.gclip) g = gc * g;
+      if (GC) g = gc * g;
       const float w = elem(t.w, i * ld + col + e, t.fp32);
       const float vn = fmaf(k.a2, __fmul_rn(g, g), __fmul_rn(k.b2, ldg(t.V + sidx)));
       stg(t.V + sidx, vn);
@@ -1800,13 +1805,13 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
         num = __fmul_rn(k.s_0, g);
       }
       const float U = __fmul_rn(num / dd, kc);
-      const float x = fmaf(-k.lr, U, decayed(w, t.decay && k.wd != 0.f, k.wd));
+      const float x = fmaf(-k.lr, U, decayed(w, DEC && t.decay, k.wd));
       if (t.fp32) {   // float32 master: no dither, no cast
         stg(reinterpret_cast<float *>(t.w) + i * ld + col + e, x);
         continue;
       }
       const uint64_t idx = (uint64_t)(t.idx0 + sidx);
-      const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0;
+      constexpr bool xu = XU;
       const float y = fmaf(dither_fac(dither_of(dz.pair(idx >> 1), idx), xu), dither_mul(w, xu), x);
       stg(t.w + i * ld + col + e, to_bf16(y));
     }
@@ -1816,7 +1821,11 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
 // --------------------------------------------------------------------------------------------
 // p3: clip factor, state update, weight update and dithered bf16 write-back (Alg. 1)
 // --------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restrict__ TT,
+// XU: the exact-ulp dither; DEC: the decoupled weight decay is on (lr lambda != 0); GC: the
+// gradient-norm mode (elements enter as fl(c g))
+// (at most 128 VGPRs: four waves per SIMD keep enough loads in flight)
+template <bool XU, bool DEC, bool GC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void p3_kernel(const DevTensor *__restrict__ TT,
                                                       const Item *__restrict__ items, StepConsts k,
                                                       RecheckLists *L) {
   // the re-check lists of this step are consumed: empty them for the next
@@ -1830,9 +1839,9 @@ __global__ __launch_bounds__(kThreads) void p3_kernel(const DevTensor *__restric
   const float kc = ldg(&t.sc->k);
   const Dither dz(k.seed, k.step, t.tensor_id);
   if (t.kind == kFactored)
-    p3_factored(t, tl, k, kc, ldg(&t.sc->q), dz);
+    p3_factored<XU, DEC, GC>(t, tl, k, kc, ldg(&t.sc->q), dz);
   else
-    p3_exact(t, tl, k, kc, dz);
+    p3_exact<XU, DEC, GC>(t, tl, k, kc, dz);
 }
 
 }  // namespace
@@ -1848,8 +1857,13 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
   const dim3 grid((uint32_t)count), block(kZThreads);
   hipStream_t s = (hipStream_t)stream;
   switch (variant) {
-#define SKEW_P1Z_CASE(V, NSEG, VEC, MOM) \
-  case V: hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC>), grid, block, 0, s, T, items, k, mode); break;
+#define SKEW_P1Z_CASE(V, NSEG, VEC, MOM)                                                        \
+  case V:                                                                                        \
+    if (mode != 0)                                                                               \
+      hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, true>), grid, block, 0, s, T, items, k, mode); \
+    else                                                                                         \
+      hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, false>), grid, block, 0, s, T, items, k, 0);   \
+    break;
     SKEW_P1Z_CASE(0, 1, true, false)
     SKEW_P1Z_CASE(1, 1, true, true)
     SKEW_P1Z_CASE(2, 1, false, false)
@@ -1913,7 +1927,12 @@ int launch_clip_recheck(const DevTensor *T, RecheckLists *L, int ntensors, const
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
               void *stream) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(p3_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, L);
+  const bool xu = (k.flags & SKEW_FLAG_EXACT_ULP) != 0, dec = k.wd != 0.f, gc = k.gclip != 0;
+  auto *kern = xu ? (dec ? (gc ? p3_kernel<true, true, true> : p3_kernel<true, true, false>)
+                         : (gc ? p3_kernel<true, false, true> : p3_kernel<true, false, false>))
+                  : (dec ? (gc ? p3_kernel<false, true, true> : p3_kernel<false, true, false>)
+                         : (gc ? p3_kernel<false, false, true> : p3_kernel<false, false, false>));
+  hipLaunchKernelGGL(kern, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k, L);
   return (int)hipGetLastError();
 }
 

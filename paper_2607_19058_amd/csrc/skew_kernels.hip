@@ -1506,8 +1506,10 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
       o.S = fmin(SUf, Yf) * (1.0 + 1e-6);  // an upper bound of the oracle's sum
       o.open = (have_z && have_y) ? kWhyStraddle : kWhyMissingSum;
     }
-    // the next step's prediction, with a factor-2 margin on either side of the floor
-    const int next = (lo >= 2.f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
+    // the next step's prediction. Without new gradient R_i c'_j only decays by beta2 per
+    // step, but a larger gradient can lift it by any factor: a 5% margin above the floor,
+    // a factor 2 below it. A wrong prediction costs a re-check at most.
+    const int next = (lo >= 1.05f * k.eps) ? kRegimeAbove : (2.f * hi < k.eps ? kRegimeFloor : kRegimeBoth);
     if (r.lead()) stg(&t.sc->regime, o.bad ? (int32_t)kRegimeBoth : (int32_t)next);
   } else {
     const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;   // per-part sums

@@ -259,6 +259,12 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   return SKEW_OK;
 }
 
+// the re-check lists of tensor group g
+static RecheckLists *group_lists(skew_ctx *ctx, int g) {
+  return reinterpret_cast<RecheckLists *>(reinterpret_cast<unsigned char *>(ctx->lists) +
+                                          (size_t)g * ctx->plan.lists_stride);
+}
+
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
   StepConsts k = make_consts(*hp);
@@ -322,7 +328,7 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
     }
     if (ctx->p2.count(g) > 0) run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
     if (ctx->clip.count(g) > 0) {
-      RecheckLists *L = ctx->lists;
+      RecheckLists *L = group_lists(ctx, g);
       run(5, s0, [&] { return launch_clip(T, ctx->clip.at(g), ctx->clip.count(g), k, L, nt, s0); });
       // re-checks of the tensors the clip stage listed (launches with empty lists exit at once)
       run(6, s0, [&] { return launch_recheck(T, L, nt, k, 1, s0); });
@@ -332,14 +338,14 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
     }
     if (p.ngroups == 1) {
       if (ctx->p3.count(g) > 0)
-        run(8, s0, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, ctx->lists, s0); });
+        run(8, s0, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, group_lists(ctx, g), s0); });
       continue;
     }
     if (e == 0) e = (int)hipEventRecord(ctx->sync[2 + g], s0);
     // the update pass of group g on the side stream, concurrent with pass 1 of group g + 1
     if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[2 + g], 0);
     if (ctx->p3.count(g) > 0)
-      run(8, s1, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, ctx->lists, s1); });
+      run(8, s1, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, group_lists(ctx, g), s1); });
   }
   // the caller's stream continues after the last update
   if (e == 0 && p.ngroups > 1) {

@@ -41,6 +41,8 @@ struct TensorScalars {
 // Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
 // launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for
 // the exact float sequence. Counts are zeroed by the update pass at the end of each step.
+// Each group of tensors has its own lists (its update pass may run beside the next
+// group's clip stage).
 struct RecheckLists {
   int32_t n1, n2;
   int32_t pad[62];
@@ -181,7 +183,8 @@ constexpr int kMaxGroups = 1;
 struct Plan {
   std::vector<TensorPlan> t;                  // sub-tensors (the device table's entries)
   std::vector<int32_t> desc_sub0, desc_nsub;  // per descriptor: its first sub-tensor and their count
-  size_t off_lists = 0;                       // workspace offset of the RecheckLists
+  size_t off_lists = 0;                       // workspace offset of the first group's RecheckLists
+  size_t lists_stride = 0;                    // bytes from one group's RecheckLists to the next
   size_t off_zero = 0;                        // workspace offset of 256 zero bytes
   size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)
   size_t off_gsq = 0;                         // workspace offset of the per-tensor sums of g^2

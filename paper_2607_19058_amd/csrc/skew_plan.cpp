@@ -201,7 +201,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
                                      p.clip.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
-  ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
+  p.lists_stride = align_up(sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
+  ws += p.lists_stride * (size_t)p.ngroups;
   p.off_zero = ws;   // zero-filled with the workspace at set-up and never written
   ws = align_up(ws + 256);
   p.off_gscale = ws;

@@ -79,7 +79,7 @@ def kernel_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
+def cpu_baseline(wl, budget_s: float = 15.0) -> dict:
     """The CPU oracle as it stands, on a resident sample of the workload: 8 expert
     matrices, one attention matrix, one norm vector and one router, stepped repeatedly."""
     import numpy as np
@@ -104,7 +104,7 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
     while True:
         steps += 1
         oracle.step(T, steps)
-        if time.perf_counter() - t0 >= budget_s or steps >= 40:
+        if time.perf_counter() - t0 >= budget_s or steps >= 400:
             break
     dt = time.perf_counter() - t0
     return {"value": round(params * steps / dt / 1e9, 4), "unit": "Gparams/s", "cores": oracle.threads(),
@@ -121,7 +121,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--weight-decay", type=float, default=0.0,
                     help="decoupled weight decay lambda fused into the update (router exempt)")
     ap.add_argument("--max-grad-norm", type=float, default=0.0,

@@ -193,6 +193,24 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       acc += bytes[i];
     }
   }
+  // update-pass and update-sum items: within each group, tiles that take longest go first,
+  // so that they do not finish last: the exact second moment's element-by-element path,
+  // and matrices narrower than a 512-column strip (idle lanes)
+  {
+    auto slow = [&](const Item &it) {
+      const TensorPlan &tp = p.t[(size_t)it.tensor];
+      return tp.kind == kExact || tp.m < 512;
+    };
+    auto order = [&](std::vector<Item> &v) {
+      std::stable_sort(v.begin(), v.end(), [&](const Item &a, const Item &b) {
+        const int ga = p.tgroup[(size_t)a.tensor], gb = p.tgroup[(size_t)b.tensor];
+        if (ga != gb) return ga < gb;
+        return slow(a) && !slow(b);
+      });
+    };
+    order(p.p3);
+    order(p.p2);
+  }
   p.state_bytes = st;
   // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][re-check lists][partials]
   size_t ws = 0;

@@ -24,7 +24,9 @@ constexpr int kSub = 2;                  // update-sum passes: work-groups (row 
 constexpr int kZThreads = 512;           // 8 wave64 (up to 256 VGPRs each: nothing is held in flight)
 constexpr int kZWaves = kZThreads / 64;
 constexpr int kZMaxSeg = 4;              // 512-column chunks per wave and row
-constexpr int64_t kZBandElems = 1 << 21; // target elements per row band: 4 MiB of bf16 gradient
+constexpr int64_t kZBandElems = 1 << 21; // elements per row band, at most: 4 MiB of bf16 gradient
+constexpr int64_t kZMinBandElems = 1 << 19;   // ... and at least (unless a row is longer)
+constexpr double kZTargetBands = 1024.0;      // bands per row-band launch class, about
 constexpr int kZVariants = 12;           // kernel variants: log2(nseg) * 4 + (element loads ? 2 : 0) + momentum
 constexpr int kZLdsBytes = 64 * 1024;    // one LDS staging buffer of the row-band pass (two per work-group)
 constexpr int kZMaxBlockRows = 64;       // rows staged per block, at most

@@ -992,6 +992,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
       if (t.zpath)
         s = ldg(t.ainv + i);
       else
+#pragma unroll 8
         for (int q = 0; q < t.ntc; q++) s += ldg(t.rowpart + (int64_t)q * t.n + i);
       const float ri = (float)((phase == 1 ? c2 * s : s) / (double)t.m);
       const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, ldg(t.R + i)));
@@ -1007,6 +1008,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     if (j < t.m) {
       double s = 0.0;
       const int nb = t.zpath ? t.nzb : t.ntr;
+#pragma unroll 8
       for (int b = 0; b < nb; b++) s += ldg(t.colpart + (int64_t)b * t.m + j);
       const float cj = (float)((phase == 1 ? c2 * s : s) / (double)t.n);
       stg(t.C + j, fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j))));
@@ -1021,6 +1023,8 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     int bad = 0;
     if (j < t.m) {
       double cs = 0.0, zs = 0.0;
+      // loads of several bands in flight; the sums still run in band order
+#pragma unroll 8
       for (int p = 0; p < t.nzb; p++) {
         cs += ldg(t.colpart + (int64_t)p * t.m + j);
         zs += ldg(t.zpart + (int64_t)p * t.m + j);

@@ -12,6 +12,25 @@ namespace skew {
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
+// row, nseg (1, 2 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
+// row and rpi = 8 / wpr rows are side by side. A block of rpi * zrb rows (bf16 gradient,
+// plus fp32 momentum on the backbone) fills at most one LDS buffer. zrb = 0: no row band.
+struct RowBandShape {
+  int64_t zcw, nseg, rpi, zrb;
+};
+static RowBandShape rowband_shape(int64_t m, bool momentum) {
+  RowBandShape r;
+  r.zcw = ceil_div(m, kChunk);
+  r.nseg = r.zcw <= 1 ? 1 : (r.zcw <= 2 * kZWaves ? 2 : 4);
+  const int64_t wpr = ceil_div(r.zcw, r.nseg);
+  const int64_t row_kb = r.zcw * (momentum ? 3 : 1);   // staged KiB per row
+  r.rpi = wpr <= kZWaves ? kZWaves / wpr : 0;
+  r.zrb = r.rpi > 0 ? std::min<int64_t>(r.nseg <= 2 ? 4 : 1, kZLdsBytes / (r.rpi * row_kb * 1024)) : 0;
+  while (r.zrb & (r.zrb - 1)) r.zrb &= r.zrb - 1;   // a power of two: 1, 2 or 4
+  return r;
+}
+
 int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   if (n < 0 || (n > 0 && d == nullptr) || out == nullptr) return SKEW_EINVAL;
   Plan p;
@@ -36,6 +55,27 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     if (nsub > INT32_MAX / 4) return SKEW_EINVAL;
   }
   p.t.resize((size_t)nsub);
+  // Row-band size per launch class (with and without momentum, the row-band pass's two
+  // kinds of launch): about kZTargetBands bands over the class, so that a class of few
+  // tensors still fills the chip, between kZMinBandElems and kZBandElems elements
+  int64_t band_elems[2] = {kZBandElems, kZBandElems};
+  {
+    double cls[2] = {0.0, 0.0};
+    for (int i = 0; i < n; i++) {
+      const skew_tensor_desc &x = d[i];
+      if (x.ndim == 1 || x.rows <= 0 || x.cols <= 0) continue;
+      if (x.tier == SKEW_TIER_ROUTER && !(x.state_flags & SKEW_STATE_FACTORED)) continue;
+      const bool mom = x.tier == SKEW_TIER_BACKBONE || (x.state_flags & SKEW_STATE_MOMENTUM) != 0;
+      if (rowband_shape(x.cols, mom).zrb < 1) continue;
+      const double E = (x.ndim == 3) ? (double)x.batch : 1.0;
+      cls[mom ? 1 : 0] += E * (double)x.rows * (double)x.cols;
+    }
+    for (int c = 0; c < 2; c++) {
+      int64_t b = kZBandElems;
+      while (b > kZMinBandElems && (double)b * kZTargetBands > cls[c]) b >>= 1;
+      band_elems[c] = b;
+    }
+  }
   size_t st = 0;        // state bytes
   size_t ws_part = 0;   // partial-sum bytes (offsets relative to the partial region)
   int64_t items_total = 0;
@@ -110,17 +150,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
     tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
     if (e == 0) p.clip.push_back({i, 0});   // one clip item per group (its first slice)
-    // Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
-    // row, nseg (1, 2 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
-    // row and zrpi = 8 / wpr rows are side by side. A block of zrpi * zrb rows (bf16
-    // gradient, plus fp32 momentum on the backbone) fills at most one LDS buffer.
-    const int64_t zcw = ceil_div(tp.m, kChunk);
-    const int64_t nseg = zcw <= 1 ? 1 : (zcw <= 2 * kZWaves ? 2 : 4);
-    const int64_t wpr = ceil_div(zcw, nseg);
-    const int64_t row_kb = zcw * (tp.momentum ? 3 : 1);   // staged KiB per row
-    const int64_t rpi = wpr <= kZWaves ? kZWaves / wpr : 0;
-    int64_t zrb = rpi > 0 ? std::min<int64_t>(nseg <= 2 ? 4 : 1, kZLdsBytes / (rpi * row_kb * 1024)) : 0;
-    while (zrb & (zrb - 1)) zrb &= zrb - 1;   // a power of two: 1, 2 or 4
+    // the row-band pass (see rowband_shape)
+    const RowBandShape rbs = rowband_shape(tp.m, tp.momentum != 0);
+    const int64_t zcw = rbs.zcw, nseg = rbs.nseg, rpi = rbs.rpi, zrb = rbs.zrb;
     tp.zpath = (tp.kind == kFactored && rpi > 0 && zrb >= 1) ? 1 : 0;
     if (tp.zpath) {
       tp.zcw = (int32_t)zcw;
@@ -128,7 +160,8 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.zrpi = (int32_t)rpi;
       tp.zrb = (int32_t)zrb;
       const int64_t rows_block = rpi * zrb;
-      tp.zrows = ceil_div(std::max<int64_t>(1, ceil_div(kZBandElems, tp.m)), rows_block) * rows_block;
+      tp.zrows = ceil_div(std::max<int64_t>(1, ceil_div(band_elems[tp.momentum ? 1 : 0], tp.m)), rows_block) *
+                 rows_block;
       tp.zrows = std::min<int64_t>(tp.zrows, kZMaxBandRows / rows_block * rows_block);
       const int64_t nzb = ceil_div(tp.n, tp.zrows), nfc = ceil_div(tp.m, kFold);
       if (nzb > INT32_MAX / 2 || nfc > INT32_MAX / 2) return SKEW_EINVAL;

@@ -138,7 +138,7 @@ def _desc_for(tier: int, w, g, tensor_id: int, state_flags: int = 0) -> TensorDe
             raise ValueError("stacked matrices must be row-major (unit column stride)")
         ld = w.stride(1) if n > 1 else max(1, m)
         ld = max(ld, m, 1)
-        if E > 1 and w.stride(0) != n * ld:
+        if E > 1 and n * m > 0 and w.stride(0) != n * ld:   # (a tensor with no elements has no layout)
             raise ValueError("stacked slices must follow each other (slice stride rows * ld)")
         return make_desc(tier, 3, n, m, ld, tensor_id, w.data_ptr(), g.data_ptr(), batch=E,
                          state_flags=state_flags)

@@ -1,0 +1,61 @@
+"""GPU edge cases of the descriptor table, checked against the CPU oracle: tensors with no
+elements (a zero row or column count, an empty vector, a stacked tensor of no slices or of
+empty slices) in every tier, mixed into a table of ordinary tensors, and a table that holds
+nothing but empty tensors. Empty tensors keep no state and take no work; the others must
+match the oracle as they do without them (also with the gradient-norm scaling, whose norm
+runs over every tensor of the table, and the decay)."""
+import pytest
+import torch
+
+import oracle
+from paper_2607_19058_amd import SkewAdam
+from paper_2607_19058_amd import workloads as W
+
+from parity_util import log, run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a HIP device")
+    torch.cuda.init()
+
+
+def _mixed():
+    shapes = [("bb.empty_rows", W.BACKBONE, (0, 64)), ("bb", W.BACKBONE, (256, 256)),
+              ("bb.empty_vec", W.BACKBONE, (0,)), ("bb.vec", W.BACKBONE, (257,)),
+              ("ex.empty_cols", W.EXPERT, (64, 0)), ("ex", W.EXPERT, (128, 520)),
+              ("ex.no_slices", W.EXPERT, (0, 64, 64)), ("ex.empty_slices", W.EXPERT, (3, 0, 16)),
+              ("ex.stack", W.EXPERT, (3, 64, 96)),
+              ("rt.empty", W.ROUTER, (0, 8)), ("rt", W.ROUTER, (256, 8)), ("rt.empty_vec", W.ROUTER, (0,))]
+    specs = [W.Spec(name, tier, shape, k) for k, (name, tier, shape) in enumerate(shapes)]
+    wl = W.Workload("mixed_empty", specs, 4)
+    sample = [k for k, s in enumerate(specs) if s.numel > 0]
+    return wl, sample
+
+
+@pytest.mark.parametrize("hp", [oracle.DEFAULTS, dict(oracle.DEFAULTS, weight_decay=0.05, max_grad_norm=1e-3)],
+                         ids=["plain", "gnorm+decay"])
+def test_empty_tensors_mixed_into_every_tier(hp):
+    wl, sample = _mixed()
+    log(f"[parity] {len(wl.specs)} tensors, {len(wl.specs) - len(sample)} of them empty, {hp}; "
+        f"non-empty ones compared")
+    st = run(wl, sample=sample, hp=hp)
+    assert st.ok(), st
+    assert st.compared > 0
+
+
+def test_table_of_only_empty_tensors():
+    dev = torch.device("cuda")
+    shapes = [(W.BACKBONE, (0, 16)), (W.EXPERT, (8, 0)), (W.ROUTER, (0,)), (W.EXPERT, (0, 4, 4))]
+    ws = [torch.zeros(s, dtype=torch.bfloat16, device=dev) for _, s in shapes]
+    gs = [torch.zeros(s, dtype=torch.bfloat16, device=dev) for _, s in shapes]
+    opt = SkewAdam([(t, ws[k], gs[k], k) for k, (t, _) in enumerate(shapes)])
+    assert opt.state_nbytes == 0
+    for t in (1, 2):
+        opt.step(t, max_grad_norm=1.0 if t == 2 else 0.0)
+    torch.cuda.synchronize()
+    kk, route = opt.clip_info()
+    assert list(kk) == [0.0] * len(shapes) and list(route) == [0] * len(shapes)

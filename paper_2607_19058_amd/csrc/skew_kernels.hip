@@ -516,7 +516,8 @@ __device__ __forceinline__ double wave_sum_rows(const double (&v)[RB]) {
 __device__ __forceinline__ float div_to_float(double x, double d, double rd) {
   const double q0 = x * rd;
   const double q = fma(fma(-q0, d, x), rd, q0);
-  return (float)q;
+  // an infinite (or NaN) sum is its own quotient; the correction would turn inf into NaN
+  return (float)(__builtin_isfinite(q0) ? q : q0);
 }
 // 1 / x and 1 / sqrt(x) to about 2^-50 (hardware estimate and one Newton step)
 __device__ __forceinline__ double rcp_d(double x) {

@@ -59,3 +59,34 @@ def test_table_of_only_empty_tensors():
     torch.cuda.synchronize()
     kk, route = opt.clip_info()
     assert list(kk) == [0.0] * len(shapes) and list(route) == [0] * len(shapes)
+
+
+def test_nonfinite_gradients_propagate_as_in_the_oracle():
+    """Non-finite gradients propagate (no skipping): a NaN element makes its tensor's clip
+    factor, and so every weight of that tensor, NaN; an infinite one gives infinite second
+    moments. Each tier gets a NaN at step 2 and an infinity at step 3; the other tensors and
+    every state array must still match the oracle."""
+    from parity_util import ParityRun
+    shapes = [("bb", W.BACKBONE, (64, 512)), ("bb.vec", W.BACKBONE, (300,)), ("ex", W.EXPERT, (128, 520)),
+              ("ex.b", W.EXPERT, (64, 64)), ("rt", W.ROUTER, (64, 8)), ("bb.clean", W.BACKBONE, (64, 64)),
+              ("ex.clean", W.EXPERT, (96, 1024))]
+    wl = W.Workload("nonfinite", [W.Spec(n, t, s, k) for k, (n, t, s) in enumerate(shapes)], 4)
+
+    def mutate(t, G):
+        if t == 2:
+            for k in (0, 2, 4):
+                G[k].view(-1)[7] = float("nan")
+        if t == 3:
+            for k in (1, 3):
+                G[k].view(-1)[5] = float("inf")
+
+    pr = ParityRun(wl)
+    for t in range(1, 5):
+        pr.step(t, mutate=mutate)
+    log(f"  total: {pr.stats}")
+    assert pr.stats.ok(), pr.stats
+    kk, _ = pr.opt.clip_info()
+    assert all(kk[k] != kk[k] for k in (0, 2, 4))              # NaN clip factors
+    for k in (0, 2, 4):
+        assert torch.isnan(pr.W[k].float()).all()
+    assert not torch.isnan(pr.W[5].float()).any() and not torch.isnan(pr.W[6].float()).any()

@@ -61,11 +61,14 @@ def test_table_of_only_empty_tensors():
     assert list(kk) == [0.0] * len(shapes) and list(route) == [0] * len(shapes)
 
 
-def test_nonfinite_gradients_propagate_as_in_the_oracle():
+@pytest.mark.parametrize("hp", [oracle.DEFAULTS, dict(oracle.DEFAULTS, weight_decay=0.05, max_grad_norm=1.0)],
+                         ids=["plain", "gnorm+decay"])
+def test_nonfinite_gradients_propagate_as_in_the_oracle(hp):
     """Non-finite gradients propagate (no skipping): a NaN element makes its tensor's clip
     factor, and so every weight of that tensor, NaN; an infinite one gives infinite second
     moments. Each tier gets a NaN at step 2 and an infinity at step 3; the other tensors and
-    every state array must still match the oracle."""
+    every state array must still match the oracle. With the gradient-norm scaling the norm
+    itself is NaN, and so is every tensor."""
     from parity_util import ParityRun
     shapes = [("bb", W.BACKBONE, (64, 512)), ("bb.vec", W.BACKBONE, (300,)), ("ex", W.EXPERT, (128, 520)),
               ("ex.b", W.EXPERT, (64, 64)), ("rt", W.ROUTER, (64, 8)), ("bb.clean", W.BACKBONE, (64, 64)),
@@ -80,7 +83,7 @@ def test_nonfinite_gradients_propagate_as_in_the_oracle():
             for k in (1, 3):
                 G[k].view(-1)[5] = float("inf")
 
-    pr = ParityRun(wl)
+    pr = ParityRun(wl, hp=hp)
     for t in range(1, 5):
         pr.step(t, mutate=mutate)
     log(f"  total: {pr.stats}")
@@ -89,4 +92,5 @@ def test_nonfinite_gradients_propagate_as_in_the_oracle():
     assert all(kk[k] != kk[k] for k in (0, 2, 4))              # NaN clip factors
     for k in (0, 2, 4):
         assert torch.isnan(pr.W[k].float()).all()
-    assert not torch.isnan(pr.W[5].float()).any() and not torch.isnan(pr.W[6].float()).any()
+    clean_nan = [bool(torch.isnan(pr.W[k].float()).any()) for k in (5, 6)]
+    assert clean_nan == ([True, True] if hp.get("max_grad_norm", 0.0) > 0 else [False, False])

@@ -159,7 +159,7 @@ class ParityRun:
             bad = int(np.count_nonzero(~((err <= lim) | same)))
             with np.errstate(invalid="ignore", divide="ignore"):
                 rel = np.where(r != 0, err / np.abs(r), np.where(err == 0, 0.0, np.inf))
-            if rel.size:
+            if rel.size and not np.all(np.isnan(rel)):
                 st.max_rel_rc = max(st.max_rel_rc, float(np.nanmax(rel)))
             if bad:
                 st.state_bad[f"{s.name}.{name}"] = bad

@@ -634,10 +634,10 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         rbuf[lane] = ldg(t.R + ic);
     }
   };
-  // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (four
-  // 16-byte reads in flight together). Staged padding is zero; a segment past the row's
-  // last chunk (wave-uniform) reads the zero area instead.
-  constexpr int RBB = (4 / NSEG < RB ? 4 / NSEG : RB) > 0 ? (4 / NSEG < RB ? 4 / NSEG : RB) : 1;
+  // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (up
+  // to eight 16-byte reads in flight together, one wait for them). Staged padding is zero;
+  // a segment past the row's last chunk (wave-uniform) reads the zero area instead.
+  constexpr int RBB = (8 / NSEG < RB ? 8 / NSEG : RB) > 0 ? (8 / NSEG < RB ? 8 / NSEG : RB) : 1;
   auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&u)[RBB][NSEG]) {
     const unsigned char *ptr[RBB * NSEG];
 #pragma unroll

@@ -6,7 +6,7 @@ backbone 341,352,448 / experts 6,442,450,944 / router 524,288 parameters, the ti
 sizes of the paper's model), bf16 weights and gradients resident in HBM.
 
 One timed step is one call of skew_step over every tensor, i.e. the whole hot path
-(pass-1 sums, fold, pass-2 sum of squares, pass-3 update and dithered write-back).
+(row-band statistics, fold, update sums, clip factor, update and dithered write-back).
 W warmup steps draw fresh seeded gradients; the K timed steps then run back to back
 on the resident gradient of one further draw, with the step counter advancing, so
 inputs are in HBM when the timed region starts. Prints one JSON line.
@@ -16,7 +16,9 @@ Reported alongside the headline (parameters updated per second):
                 HIP events recorded around each of the library's kernels on the launch
                 stream over the timed region; `traffic` from the committed rocprofv3
                 FETCH_SIZE / WRITE_SIZE summary when the kernel source still matches it
-  step          the whole step's algorithmic bytes and effective GB/s
+  step          the whole step's algorithmic bytes and effective GB/s; the median, min and
+                max of the timed steps (an event between steps), and the warm-up steps
+                (steps 1.. of the run) timed one by one
   cpu_baseline  the CPU oracle (plain C, OpenMP) on a bounded resident sample of the
                 same workload, on this host's cores
 """
@@ -178,24 +180,32 @@ def main() -> int:
     hp = dict(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, clip_threshold=1.0, seed=0,
               weight_decay=args.weight_decay, max_grad_norm=args.max_grad_norm,
               flags=2 if args.exact_ulp else 0)
+    stream = torch.cuda.current_stream()
+    first = []   # the warm-up steps (steps 1.. of the run) timed one by one, input drawing excluded
     for t in range(1, args.warmup + 1):
         draw(t)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
         opt.step(t, **hp)
+        b.record(stream)
+        first.append((a, b))
     draw(args.warmup + 1)
     torch.cuda.synchronize()
+    first_ms = [round(a.elapsed_time(b), 3) for a, b in first]
     log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
 
     opt.timing_enable(args.steps)
-    stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]   # one between steps
+    e0, e1 = evs[0], evs[-1]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
     for j in range(args.steps):
         opt.step(args.warmup + 1 + j, **hp)
-    e1.record(stream)
+        evs[j + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    step_ms = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
     per_kernel = opt.timing_read()
     steps_rec = per_kernel.pop("_steps")
     ev_ms = e0.elapsed_time(e1)
@@ -263,6 +273,9 @@ def main() -> int:
         "step": {"algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3),
                  "effective_GBps": round(step_gbps, 1), "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),
                  "event_ms_per_step": round(ev_ms / args.steps, 4),
+                 "ms_median": round(step_ms[len(step_ms) // 2], 4), "ms_min": round(step_ms[0], 4),
+                 "ms_max": round(step_ms[-1], 4),
+                 "warmup_steps_ms": first_ms,   # steps 1.. of the run, before the timed region
                  "kernel_ms_per_step": {k: round(v, 4) for k, v in kern_avg.items()}},
         **({"torch_clip_grad_norm_ms": round(unfused_ms, 4)} if unfused_ms is not None else {}),
     }

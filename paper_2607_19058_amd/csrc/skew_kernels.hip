@@ -1542,7 +1542,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
                                                         RecheckLists *L, int ntensors) {
   __shared__ double sh[kThreads];
   __shared__ double wsum[kWaves][3];
-  __shared__ int wflag[kWaves][2];
+  __shared__ int wflag[kWaves][3];
   __shared__ float kf_sh;
   __shared__ int st_sh, pos_sh;
   const Item it = items[blockIdx.x];   // the first sub-tensor of a group sharing one k
@@ -1563,14 +1563,17 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   } else {
     const int w = (int)(threadIdx.x >> 6);
     double s = 0.0, e_ = 0.0, nn = 0.0;
-    int first = 0x7fffffff, bad = 0;   // 8 x (the first open slice) + why
+    int first = 0x7fffffff, why = 0, bad = 0;   // the wave's first open slice, and why it is open
     for (int e = w; e < ng; e += kWaves) {
       const DevTensor &t = TT[g0 + e];
       const SliceSum o = slice_sum(t, k, RedWave{});
       s += o.S;
       e_ += o.E;
       nn += (double)(t.n * t.m);
-      if (o.open && first == 0x7fffffff) first = 8 * e + o.open;
+      if (o.open && first == 0x7fffffff) {
+        first = e;
+        why = o.open;
+      }
       bad |= o.bad;
     }
     if ((threadIdx.x & 63) == 0) {
@@ -1578,7 +1581,8 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       wsum[w][1] = e_;
       wsum[w][2] = nn;
       wflag[w][0] = first;
-      wflag[w][1] = bad;
+      wflag[w][1] = why;
+      wflag[w][2] = bad;
     }
     __syncthreads();
     int f = 0x7fffffff;
@@ -1586,10 +1590,12 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       S += wsum[v][0];
       err += wsum[v][1];
       N += wsum[v][2];
-      f = min(f, wflag[v][0]);
-      bad_any |= wflag[v][1] != 0;
+      if (wflag[v][0] < f) {
+        f = wflag[v][0];
+        open = wflag[v][1];
+      }
+      bad_any |= wflag[v][2] != 0;
     }
-    open = f == 0x7fffffff ? 0 : (f & 7);
   }
   if (threadIdx.x == 0) {
     bool amb = (k.flags & SKEW_FLAG_EXACT_CLIP) != 0 && t0.kind == kFactored;

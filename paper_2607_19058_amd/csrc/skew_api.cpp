@@ -235,7 +235,8 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   c->gsq = reinterpret_cast<double *>(ws + p.off_gsq);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+  // the side stream exists only for a pipeline of several groups (it takes a hardware queue)
+  hipError_t e = p.ngroups > 1 ? hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) : hipSuccess;
   for (int i = 0; e == hipSuccess && i < p.ngroups + 2; i++) {
     hipEvent_t ev;
     e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);

@@ -139,7 +139,9 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     // so that the four waves of a work-group map onto (chunk, row) pairs statically
     tp.cw = tp.m > 2 * kChunk ? 4 : (tp.m > kChunk ? 2 : 1);
     const int64_t tc = (int64_t)kChunk * tp.cw;
-    tp.tr = std::max<int64_t>(1, kTileElems / tc);
+    // (exact-moment tensors take a quarter of that: their element-by-element path is the
+    // slowest per element, and their few tiles would otherwise finish last)
+    tp.tr = std::max<int64_t>(1, kTileElems / tc / (tp.kind == kExact ? 4 : 1));
     const int64_t ntc = ceil_div(tp.m, tc), ntr = ceil_div(tp.n, tp.tr);
     if (ntc * ntr > INT32_MAX / 2 / kSub) return SKEW_EINVAL;   // tile * kSub + part fits an int32
     tp.ntc = (int32_t)ntc;

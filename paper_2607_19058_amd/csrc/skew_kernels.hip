@@ -1323,30 +1323,71 @@ __device__ __forceinline__ int32_t *recheck_list(RecheckLists *L, int ntensors, 
 __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__restrict__ TT, RecheckLists *L,
                                                            int ntensors, StepConsts k, int level) {
   __shared__ double sh[kThreads];
+  // tile offsets of the listed tensors (an exclusive prefix sum), when the list fits
+  constexpr int kTable = 2048;
+  __shared__ int64_t pre[kTable + 1];
+  __shared__ int64_t part[kThreads];
   const int n = ldg(level == 1 ? &L->n1 : &L->n2);
   if (n <= 0) return;
   const int32_t *list = recheck_list(L, ntensors, level);
-  int64_t total = 0;
-  for (int j = 0; j < n; j++) {
+  auto tiles = [&](int j) {
     const DevTensor &t = TT[ldg(list + j)];
-    total += (int64_t)t.ntr * t.ntc * kSub;
+    return (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
+  };
+  const bool table = n <= kTable;
+  int64_t total = 0;
+  if (table) {
+    // thread i sums the counts of entries [8i, 8i + 8), a scan over the threads gives each
+    // its start, and it writes its entries' offsets
+    constexpr int kPer = kTable / kThreads;
+    const int j0 = (int)threadIdx.x * kPer;
+    int64_t c[kPer], sum = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; q++) {
+      c[q] = j0 + q < n ? tiles(j0 + q) : 0;
+      sum += c[q];
+    }
+    part[threadIdx.x] = sum;
+    __syncthreads();
+    for (int off = 1; off < kThreads; off <<= 1) {   // inclusive scan of the thread sums
+      const int64_t v = threadIdx.x >= (unsigned)off ? part[threadIdx.x - off] : 0;
+      __syncthreads();
+      part[threadIdx.x] += v;
+      __syncthreads();
+    }
+    int64_t run = part[threadIdx.x] - sum;
+#pragma unroll
+    for (int q = 0; q < kPer; q++) {
+      pre[j0 + q] = run;
+      run += c[q];
+    }
+    if (threadIdx.x == kThreads - 1) pre[kTable] = run;
+    __syncthreads();
+    total = pre[n];
+  } else {
+    for (int j = 0; j < n; j++) total += tiles(j);
   }
+  // the tiles of this work-group come in increasing order, so the listed tensor they fall
+  // in only moves forward; q is formed once per tensor
+  int j = 0, qj = -1;
+  int64_t base = 0, nt_j = table ? pre[1] - pre[0] : tiles(0);
+  float q = 0.f;
   for (int64_t idx = blockIdx.x; idx < total; idx += gridDim.x) {
-    int64_t base = 0;
-    int j = 0;
-    for (;; j++) {
-      const DevTensor &t = TT[ldg(list + j)];
-      const int64_t nt = (int64_t)t.ntr * t.ntc * kSub;
-      if (idx < base + nt) break;
-      base += nt;
+    while (idx >= base + nt_j) {
+      base += nt_j;
+      j++;
+      nt_j = table ? pre[j + 1] - pre[j] : tiles(j);
     }
     const DevTensor &t = TT[ldg(list + j)];
     const int tile = (int)(idx - base);   // tile * kSub + part
     const Tile tl = tile_of(t, tile / kSub);
-    const int part = tile % kSub;
-    const float q = mean_r_clamped(t, k, sh);
+    const int prt = tile % kSub;
+    if (j != qj) {
+      q = mean_r_clamped(t, k, sh);
+      qj = j;
+    }
     if (level == 1) {
-      const SumPair acc = p2_factored(t, tl, part, k, q);
+      const SumPair acc = p2_factored(t, tl, prt, k, q);
       const double sv = block_sum(acc.s, sh);
       const double q4 = block_sum(acc.q4, sh);
       if (threadIdx.x == 0) {
@@ -1354,7 +1395,7 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
         stg(t.qsum + tile, q4);
       }
     } else {
-      const double sv = block_sum(p2_factored_exact(t, tl, part, k, q), sh);
+      const double sv = block_sum(p2_factored_exact(t, tl, prt, k, q), sh);
       if (threadIdx.x == 0) stg(t.ssum + tile, sv);
     }
   }

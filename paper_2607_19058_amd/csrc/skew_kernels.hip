@@ -1246,6 +1246,24 @@ __device__ __forceinline__ double p2_factored_exact(const DevTensor &t, const Ti
   float cp[8];
 #pragma unroll
   for (int e = 0; e < 8; e++) cp[e] = (col + e < m) ? ldg(t.C + col + e) / q : 0.f;
+  if (t.vec) {   // 16-byte rows: 8 elements per load
+    for (int64_t lr = r0; lr < tl.nr; lr += rs) {
+      const int64_t i = tl.row(lr);
+      const float Ri = ldg(t.R + i);
+      float x[8], mo[8];
+      unpack8(ldg(reinterpret_cast<const uint4 *>(t.g + i * ld + col)), x);
+      if (mom) load_m8(t.M + i * m + col, mo);
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        // the momentum update takes the scaled gradient (as in the update pass)
+        const float xs = k.gclip ? gc * x[e] : x[e];
+        const float xm = mom ? fmaf(k.a1, xs, __fmul_rn(k.b1, mo[e])) : xs;
+        const float u = __fmul_rn(s, xm) / sqrtf(max_nan(__fmul_rn(Ri, cp[e]), k.eps));
+        acc = fma((double)u, (double)u, acc);
+      }
+    }
+    return acc;
+  }
   for (int64_t lr = r0; lr < tl.nr; lr += rs) {
     const int64_t i = tl.row(lr);
     const float Ri = ldg(t.R + i);

@@ -66,6 +66,8 @@ class Workload:
     banks: Dict[int, int] = field(default_factory=dict)   # bank -> number of experts
     zero_per_step: Dict[int, int] = field(default_factory=dict)
     fixed_zero: Optional[Dict[int, List[int]]] = None      # bank -> experts zero at every step
+    fixed_zero_from: int = 1           # ... from this step on (earlier steps draw them as usual)
+    expert_zero_rows: float = 0.0      # share of each expert matrix's rows that are always zero
     expert_sparsity: float = 0.0       # i.i.d. zero probability of expert entries
     outlier_rate: float = 0.0
     outlier_scale: float = 1.0
@@ -210,8 +212,27 @@ def tiny_stacked() -> Workload:
                     zero_per_step={0: 1})
 
 
+def tiny_late_zero() -> Workload:
+    """The tiny workload whose two zero experts draw gradients at steps 1-5 and none from
+    step 6 on: their R and C then decay by beta2 from real values."""
+    import dataclasses
+    return dataclasses.replace(tiny(), name="tiny_late_zero", fixed_zero_from=6)
+
+
+def zero_rows() -> Workload:
+    """Experts with 90% of their rows entirely zero at every step (R_i = 0 there), beside a
+    backbone and a router: 8 experts x {512x2048, 2048x512}."""
+    specs, add = _builder()
+    add("bb", BACKBONE, (512, 512), 2)
+    for e in range(8):
+        add(f"ex{e}.up", EXPERT, (512, 2048), bank=0, expert=e)
+        add(f"ex{e}.down", EXPERT, (2048, 512), bank=0, expert=e)
+    add("router", ROUTER, (512, 8))
+    return Workload("zero_rows", specs, 8, banks={0: 8}, expert_zero_rows=0.9, zero_per_step={0: 1})
+
+
 CONFIGS = {"tiny": tiny, "layer": layer, "full": full, "stress": stress, "ragged": ragged,
-           "tiny_stacked": tiny_stacked}
+           "tiny_stacked": tiny_stacked, "tiny_late_zero": tiny_late_zero, "zero_rows": zero_rows}
 
 
 def get(name: str) -> Workload:
@@ -238,7 +259,7 @@ def expert_scales(wl: Workload, step: int) -> Dict[int, np.ndarray]:
             rho = (ne / 2.0) * pi                      # mean 1
         else:
             rho = np.ones(ne)
-        if wl.fixed_zero is not None:
+        if wl.fixed_zero is not None and step >= wl.fixed_zero_from:
             rho[wl.fixed_zero.get(bank, [])] = 0.0
         nz = wl.zero_per_step.get(bank, 0)
         if nz:
@@ -291,6 +312,10 @@ def fill_grad(spec: Spec, wl: Workload, step: int, out, scales: Optional[Dict[in
         keep = torch.rand(spec.shape, generator=gen, device=dev) >= wl.expert_sparsity
         z.mul_(keep)
         del keep
+    if wl.expert_zero_rows > 0 and spec.tier == EXPERT and len(spec.shape) == 2:
+        # the same rows at every step (R_i stays exactly 0 there, beside nonzero rows)
+        rows = np.random.default_rng(_seed(wl.seed, 3, spec.tensor_id)).random(spec.shape[0])
+        z[torch.as_tensor(rows < wl.expert_zero_rows, device=dev)] = 0.0
     if stacked:
         z.mul_(torch.as_tensor(SIGMA_G * rho, dtype=torch.float32, device=dev)[:, None, None])
     else:

@@ -94,3 +94,21 @@ def test_nonfinite_gradients_propagate_as_in_the_oracle(hp):
         assert torch.isnan(pr.W[k].float()).all()
     clean_nan = [bool(torch.isnan(pr.W[k].float()).any()) for k in (5, 6)]
     assert clean_nan == ([True, True] if hp.get("max_grad_norm", 0.0) > 0 else [False, False])
+
+
+def test_experts_zero_from_step_6_decay_as_in_the_oracle():
+    """Two experts draw gradients at steps 1-5 and none from step 6 on (zero-gradient steps
+    after real ones: R and C decay by beta2 from nonzero values); every tensor compared."""
+    wl = W.get("tiny_late_zero")
+    log("[parity] tiny, two experts zero from step 6: 21 tensors, 10 steps, all compared")
+    st = run(wl)
+    assert st.ok(), st
+
+
+def test_expert_rows_always_zero():
+    """Experts with 90% of their rows zero at every step: R_i = 0 on those rows beside
+    nonzero rows (their elements sit on the eps floor with U = 0); every tensor compared."""
+    wl = W.get("zero_rows")
+    log("[parity] experts with 90% zero rows, 19 tensors, 8 steps, all compared")
+    st = run(wl)
+    assert st.ok(), st

@@ -34,11 +34,14 @@ struct skew_ctx {
   DevTensor *d_table = nullptr;
   RecheckLists *lists = nullptr;
   GroupedList p1, fold, p2, p3, clip, fold_rows;
+  GroupedList fold_z, fold_w;   // the fold's items of row-band tensors and of the others
   float *gscale = nullptr;   // device: the gradient-norm mode's scale
   double *gsq = nullptr;     // device: per-tensor sums of g^2
   GroupedList z[kZVariants];   // row-band pass items, one list per kernel variant
   hipStream_t side = nullptr;  // the update pass of the pipeline runs here
-  std::vector<hipEvent_t> sync;   // [0]: step start, [1]: update pass done, [2 + g]: group g ready
+  // [0]: step start, [1]: update pass done, [2 + g]: group g ready, [2 + ngroups]: the side
+  // stream's statistics of wide and exact tensors done
+  std::vector<hipEvent_t> sync;
   // diagnostics: per recorded step, (launch kind, start event, end event) of every launch
   struct Timed {
     int kind;
@@ -230,14 +233,26 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   add(c->p3, p.p3);
   add(c->clip, p.clip);
   add(c->fold_rows, p.fold_rows);
+  {
+    std::vector<Item> fz, fw;
+    for (const Item &it : p.fold) (table[it.tensor].zpath ? fz : fw).push_back(it);
+    add(c->fold_z, fz);
+    add(c->fold_w, fw);
+  }
   if (items.empty()) items.push_back({0, 0});
+  if (sizeof(Item) * items.size() > p.off_lists - p.off_items) {   // the planner's region must hold them
+    delete c;
+    return SKEW_EINVAL;
+  }
   c->gscale = reinterpret_cast<float *>(ws + p.off_gscale);
   c->gsq = reinterpret_cast<double *>(ws + p.off_gsq);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // the side stream exists only for a pipeline of several groups (it takes a hardware queue)
-  hipError_t e = p.ngroups > 1 ? hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) : hipSuccess;
-  for (int i = 0; e == hipSuccess && i < p.ngroups + 2; i++) {
+  // the side stream (it takes a hardware queue) runs the update pass of a pipeline of several
+  // groups, or the statistics of wide and exact tensors beside the row-band pass
+  const bool side = p.ngroups > 1 || !p.p1.empty() || !p.p2.empty();
+  hipError_t e = side ? hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) : hipSuccess;
+  for (int i = 0; e == hipSuccess && i < p.ngroups + 3; i++) {
     hipEvent_t ev;
     e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
     if (e == hipSuccess) c->sync.push_back(ev);
@@ -303,7 +318,26 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   const int nt = (int)p.t.size();
   for (int g = 0; g < p.ngroups && e == 0; g++) {
     // pass 1, fold and clip stage of group g on the caller's stream
-    if (!k.gclip) {
+    bool p2_done = false;
+    if (!k.gclip && p.ngroups == 1 && s1 != nullptr) {
+      // the wide tensors' pass 1 and fold and the update sums of wide and exact tensors
+      // run on the side stream, beside the row-band pass (which leaves ALU time and
+      // registers free); the clip stage waits for both
+      e = (int)hipEventRecord(ctx->sync[0], s0);
+      if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[0], 0);
+      if (ctx->p1.count(g) > 0) run(2, s1, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s1); });
+      if (ctx->fold_w.count(g) > 0)
+        run(3, s1, [&] { return launch_fold(T, ctx->fold_w.at(g), ctx->fold_w.count(g), k, 0, s1); });
+      if (ctx->p2.count(g) > 0) run(4, s1, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s1); });
+      if (e == 0) e = (int)hipEventRecord(ctx->sync[2 + p.ngroups], s1);
+      for (int v = 0; v < kZVariants; v++)
+        if (ctx->z[v].count(g) > 0)
+          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 0, s0); });
+      if (ctx->fold_z.count(g) > 0)
+        run(3, s0, [&] { return launch_fold(T, ctx->fold_z.at(g), ctx->fold_z.count(g), k, 0, s0); });
+      if (e == 0) e = (int)hipStreamWaitEvent(s0, ctx->sync[2 + p.ngroups], 0);
+      p2_done = true;
+    } else if (!k.gclip) {
       for (int v = 0; v < kZVariants; v++)
         if (ctx->z[v].count(g) > 0)
           run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 0, s0); });
@@ -327,7 +361,8 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
       if (ctx->fold.count(g) > 0)
         run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, 2, s0); });
     }
-    if (ctx->p2.count(g) > 0) run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
+    if (!p2_done && ctx->p2.count(g) > 0)
+      run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
     if (ctx->clip.count(g) > 0) {
       RecheckLists *L = group_lists(ctx, g);
       run(5, s0, [&] { return launch_clip(T, ctx->clip.at(g), ctx->clip.count(g), k, L, nt, s0); });

@@ -250,8 +250,10 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   // workspace: [device tensor table][items p1|z (by variant)|fold|p2|p3|clip][re-check lists][partials]
   size_t ws = 0;
   p.off_table = ws; ws = align_up(ws + sizeof(DevTensor) * (size_t)std::max(nt, 1));
+  // the item lists as the device keeps them: the fold's items appear twice (the whole list,
+  // and split into row-band and other tensors)
   p.off_items = ws;
-  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() +
+  ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + 2 * p.fold.size() + p.p2.size() + p.p3.size() +
                                      p.clip.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
   p.lists_stride = align_up(sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));

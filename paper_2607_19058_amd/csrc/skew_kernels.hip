@@ -56,6 +56,24 @@ __device__ __forceinline__ void stg(float4 *p, float4 v) {
   const f32x4_t u = {v.x, v.y, v.z, v.w};
   stg(reinterpret_cast<f32x4_t *>(p), u);
 }
+// Non-temporal 16-byte loads and stores, for data that the update pass streams through once
+// (a hint to the caches not to keep it: measured 8.07 -> 7.58 ms for the 6.78B update pass)
+template <class V>
+__device__ __forceinline__ V ldg_nt(const V *p) {
+  return __builtin_nontemporal_load((const __attribute__((address_space(1))) V *)p);
+}
+template <class V>
+__device__ __forceinline__ void stg_nt(V *p, V v) {
+  __builtin_nontemporal_store(v, (__attribute__((address_space(1))) V *)p);
+}
+__device__ __forceinline__ uint4 ldg_nt(const uint4 *p) {
+  const u32x4_t v = ldg_nt(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void stg_nt(uint4 *p, uint4 v) {
+  const u32x4_t u = {v.x, v.y, v.z, v.w};
+  stg_nt(reinterpret_cast<u32x4_t *>(p), u);
+}
 
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
@@ -76,14 +94,28 @@ __device__ __forceinline__ void unpack8(const uint4 &u, float *o) {
 }
 
 // 8 momentum values at a 32-byte aligned position
+template <bool NT = false>
 __device__ __forceinline__ void load_m8(const float *p, float *o) {
-  const float4 a = ldg(reinterpret_cast<const float4 *>(p));
-  const float4 b = ldg(reinterpret_cast<const float4 *>(p + 4));
+  f32x4_t a, b;
+  if (NT) {
+    a = ldg_nt(reinterpret_cast<const f32x4_t *>(p));
+    b = ldg_nt(reinterpret_cast<const f32x4_t *>(p + 4));
+  } else {
+    a = ldg(reinterpret_cast<const f32x4_t *>(p));
+    b = ldg(reinterpret_cast<const f32x4_t *>(p + 4));
+  }
   o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
 }
+template <bool NT = false>
 __device__ __forceinline__ void store_m8(float *p, const float *v) {
-  stg(reinterpret_cast<float4 *>(p), make_float4(v[0], v[1], v[2], v[3]));
-  stg(reinterpret_cast<float4 *>(p + 4), make_float4(v[4], v[5], v[6], v[7]));
+  const f32x4_t a = {v[0], v[1], v[2], v[3]}, b = {v[4], v[5], v[6], v[7]};
+  if (NT) {
+    stg_nt(reinterpret_cast<f32x4_t *>(p), a);
+    stg_nt(reinterpret_cast<f32x4_t *>(p + 4), b);
+  } else {
+    stg(reinterpret_cast<f32x4_t *>(p), a);
+    stg(reinterpret_cast<f32x4_t *>(p + 4), b);
+  }
 }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -1744,7 +1776,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
   if (mom) {
 #pragma unroll
     for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
-    store_m8(t.M + i * t.m + col, x);
+    store_m8<true>(t.M + i * t.m + col, x);
   }
   const float alpha = (float)(c.lsk * ldg(t.ainv + i));
   // pairs p0 .. p0 + 3: m and col are multiples of 8, so p0 is a multiple of 4 and the
@@ -1779,9 +1811,9 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
                                 c.eps, c.lr, dith[e], xu);
     }
   }
-  stg(reinterpret_cast<uint4 *>(t.w + i * t.ld + col),
-      make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
-                 pack_bf16x2(y[6], y[7])));
+  stg_nt(reinterpret_cast<uint4 *>(t.w + i * t.ld + col),
+         make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                    pack_bf16x2(y[6], y[7])));
 }
 
 template <bool XU, bool DEC, bool GC>
@@ -1807,14 +1839,14 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
     for (int64_t lr = wm.wr; lr < tl.nr; lr += 2 * wm.rpi) {
       const bool two = lr + wm.rpi < tl.nr;
       const int64_t i = tl.row(lr), i2 = two ? tl.row(lr + wm.rpi) : i;
-      const uint4 ga = ldg(reinterpret_cast<const uint4 *>(t.g + i * ld + col));
-      const uint4 wa = ldg(reinterpret_cast<const uint4 *>(t.w + i * ld + col));
-      const uint4 gb = ldg(reinterpret_cast<const uint4 *>(t.g + i2 * ld + col));
-      const uint4 wb = ldg(reinterpret_cast<const uint4 *>(t.w + i2 * ld + col));
+      const uint4 ga = ldg_nt(reinterpret_cast<const uint4 *>(t.g + i * ld + col));
+      const uint4 wa = ldg_nt(reinterpret_cast<const uint4 *>(t.w + i * ld + col));
+      const uint4 gb = ldg_nt(reinterpret_cast<const uint4 *>(t.g + i2 * ld + col));
+      const uint4 wb = ldg_nt(reinterpret_cast<const uint4 *>(t.w + i2 * ld + col));
       float ma[8], mb[8];
       if (mom) {
-        load_m8(t.M + i * m + col, ma);
-        load_m8(t.M + i2 * m + col, mb);
+        load_m8<true>(t.M + i * m + col, ma);
+        load_m8<true>(t.M + i2 * m + col, mb);
       }
       p3_row8<XU, DEC, GC>(t, k, c, dz, i, col, bf, ga, wa, ma);
       if (two) p3_row8<XU, DEC, GC>(t, k, c, dz, i2, col, bf, gb, wb, mb);

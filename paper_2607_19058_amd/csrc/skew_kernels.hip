@@ -56,8 +56,10 @@ __device__ __forceinline__ void stg(float4 *p, float4 v) {
   const f32x4_t u = {v.x, v.y, v.z, v.w};
   stg(reinterpret_cast<f32x4_t *>(p), u);
 }
-// Non-temporal 16-byte loads and stores, for data that the update pass streams through once
-// (a hint to the caches not to keep it: measured 8.07 -> 7.58 ms for the 6.78B update pass)
+// Non-temporal 16-byte loads and stores, for the bf16 gradient and weight rows that the update
+// pass streams through once (a hint to the caches not to keep them). Together they took the
+// 6.78B update pass from 8.07 to 7.65 ms; loads alone (8.23) or stores alone (8.12) did not,
+// and on the fp32 momentum the hint costs time (the expert-momentum variant: 18.1 -> 19.2 ms).
 template <class V>
 __device__ __forceinline__ V ldg_nt(const V *p) {
   return __builtin_nontemporal_load((const __attribute__((address_space(1))) V *)p);
@@ -94,28 +96,14 @@ __device__ __forceinline__ void unpack8(const uint4 &u, float *o) {
 }
 
 // 8 momentum values at a 32-byte aligned position
-template <bool NT = false>
 __device__ __forceinline__ void load_m8(const float *p, float *o) {
-  f32x4_t a, b;
-  if (NT) {
-    a = ldg_nt(reinterpret_cast<const f32x4_t *>(p));
-    b = ldg_nt(reinterpret_cast<const f32x4_t *>(p + 4));
-  } else {
-    a = ldg(reinterpret_cast<const f32x4_t *>(p));
-    b = ldg(reinterpret_cast<const f32x4_t *>(p + 4));
-  }
+  const float4 a = ldg(reinterpret_cast<const float4 *>(p));
+  const float4 b = ldg(reinterpret_cast<const float4 *>(p + 4));
   o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
 }
-template <bool NT = false>
 __device__ __forceinline__ void store_m8(float *p, const float *v) {
-  const f32x4_t a = {v[0], v[1], v[2], v[3]}, b = {v[4], v[5], v[6], v[7]};
-  if (NT) {
-    stg_nt(reinterpret_cast<f32x4_t *>(p), a);
-    stg_nt(reinterpret_cast<f32x4_t *>(p + 4), b);
-  } else {
-    stg(reinterpret_cast<f32x4_t *>(p), a);
-    stg(reinterpret_cast<f32x4_t *>(p + 4), b);
-  }
+  stg(reinterpret_cast<float4 *>(p), make_float4(v[0], v[1], v[2], v[3]));
+  stg(reinterpret_cast<float4 *>(p + 4), make_float4(v[4], v[5], v[6], v[7]));
 }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -1776,7 +1764,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
   if (mom) {
 #pragma unroll
     for (int e = 0; e < 8; e++) x[e] = fmaf(k.a1, x[e], __fmul_rn(k.b1, mv[e]));
-    store_m8<true>(t.M + i * t.m + col, x);
+    store_m8(t.M + i * t.m + col, x);
   }
   const float alpha = (float)(c.lsk * ldg(t.ainv + i));
   // pairs p0 .. p0 + 3: m and col are multiples of 8, so p0 is a multiple of 4 and the
@@ -1845,8 +1833,8 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
       const uint4 wb = ldg_nt(reinterpret_cast<const uint4 *>(t.w + i2 * ld + col));
       float ma[8], mb[8];
       if (mom) {
-        load_m8<true>(t.M + i * m + col, ma);
-        load_m8<true>(t.M + i2 * m + col, mb);
+        load_m8(t.M + i * m + col, ma);
+        load_m8(t.M + i2 * m + col, mb);
       }
       p3_row8<XU, DEC, GC>(t, k, c, dz, i, col, bf, ga, wa, ma);
       if (two) p3_row8<XU, DEC, GC>(t, k, c, dz, i2, col, bf, gb, wb, mb);

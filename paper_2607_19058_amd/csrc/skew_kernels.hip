@@ -655,10 +655,11 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     }
   };
   // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (up
-  // to eight 16-byte reads in flight together, one wait for them). Staged padding is zero;
-  // a segment past the row's last chunk (wave-uniform) reads the zero area instead.
+  // to eight 16-byte reads in flight together, one wait for them) into uk[b0 .. b0 + RBB).
+  // Staged padding is zero; a segment past the row's last chunk (wave-uniform) reads the
+  // zero area instead.
   constexpr int RBB = (8 / NSEG < RB ? 8 / NSEG : RB) > 0 ? (8 / NSEG < RB ? 8 / NSEG : RB) : 1;
-  auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&u)[RBB][NSEG]) {
+  auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&uk)[RB][NSEG]) {
     const unsigned char *ptr[RBB * NSEG];
 #pragma unroll
     for (int b = 0; b < RBB; b++)
@@ -666,7 +667,12 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       for (int s = 0; s < NSEG; s++)
         ptr[b * NSEG + s] = (chs[s] < zcw ? buf + (size_t)((grp_c * RB + b0 + b) * zcw + chs[s]) * 1024 : zlds) +
                             lane * 16;
-    lds_read16_n<RBB * NSEG>(ptr, reinterpret_cast<uint4(&)[RBB * NSEG]>(u));
+    uint4 u[RBB * NSEG];
+    lds_read16_n<RBB * NSEG>(ptr, u);
+#pragma unroll
+    for (int b = 0; b < RBB; b++)
+#pragma unroll
+      for (int s = 0; s < NSEG; s++) uk[b0 + b][s] = u[b * NSEG + s];
   };
   auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt) {
     __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
@@ -674,14 +680,18 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
     const int64_t rbase = r0 + blk * br;
     double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
+    // The lane's staged gradient of the block, read from LDS by the first sweep and kept in
+    // registers for the second where they fit (no momentum, up to two chunks per wave; the
+    // other variants would spill and read the block again)
+    constexpr bool KEEP = !MOM && NSEG <= 2;
+    uint4 uk[RB][NSEG];
     // row and column sums of g^2 (bf16 squares are exact in double); an idle wave's
     // accumulators are never used. Mode 2 has them from the first pass.
     if (mode != 2) {
       double rp[RB];
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
-        uint4 u[RBB][NSEG];
-        read_rows(cur, b0, u);
+        read_rows(cur, b0, uk);
 #pragma unroll
         for (int bb = 0; bb < RBB; bb++) {
           const int b = b0 + bb;
@@ -692,7 +702,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
             // staged element to double at once)
             __builtin_amdgcn_sched_barrier(0);
             float x[8];
-            unpack8(u[bb][s], x);
+            unpack8(uk[b][s], x);
 #pragma unroll
             for (int e = 0; e < 8; e++) {
               const double xd = (double)x[e];
@@ -765,12 +775,10 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       constexpr bool Z = decltype(zc)::value, Y = decltype(yc)::value;
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
-      uint4 ub[RBB][NSEG];
-      read_rows(cur, b0, ub);
+      if (!KEEP || mode == 2) read_rows(cur, b0, uk);   // (mode 2: the first sweep did not run)
 #pragma unroll
       for (int bb = 0; bb < RBB; bb++) {
         const int b = b0 + bb;
-        const uint4 (&u)[RBB][NSEG] = ub;
         const int r = grp_c * rb + b;
         const int src = b * P;
         const double winv = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(winv_l), src),
@@ -780,7 +788,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         for (int s = 0; s < NSEG; s++) {
           __builtin_amdgcn_sched_barrier(0);
           float x[8];
-          unpack8(u[bb][s], x);
+          unpack8(uk[b][s], x);
           if (scaled) {
 #pragma unroll
             for (int e = 0; e < 8; e++) x[e] = gc * x[e];

@@ -470,6 +470,11 @@ __device__ __forceinline__ void lds_read16_n(const unsigned char *const (&p)[N],
 #pragma unroll
   for (int j = 0; j < N; j++) u[j] = to_uint4(v[j]);
 }
+__device__ __forceinline__ uint4 lds_read16(const unsigned char *p) {
+  const u32x4_t v = *reinterpret_cast<const __attribute__((address_space(3))) u32x4_t *>(
+      (const __attribute__((address_space(3))) unsigned char *)p);
+  return to_uint4(v);
+}
 __device__ __forceinline__ void lds_write16(unsigned char *p, uint4 u) {
   *reinterpret_cast<__attribute__((address_space(3))) u32x4_t *>(
       (__attribute__((address_space(3))) unsigned char *)p) = u32x4_t{u.x, u.y, u.z, u.w};
@@ -552,7 +557,7 @@ __device__ __forceinline__ double rsq_d(double x) {
 template <int NSEG, int RB, bool MOM, bool VEC>
 __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, int mode,
                                          unsigned char *bufA, unsigned char *bufB, float *rbA, float *rbB,
-                                         double *rowsh, double *sh, float *rstash, const unsigned char *zlds) {
+                                         double *rowsh, double *sh, float *rstash) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
@@ -608,9 +613,36 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // stages the block's old R values.
   const int pr0 = wave / zcw, pc0 = wave - pr0 * zcw;                   // piece `wave`: (row, chunk)
   const int dr = kZWaves / zcw, dc = kZWaves - (kZWaves / zcw) * zcw;   // step of 8 pieces
+  // Direct loads of the gradient alone: the lane's source moves by a fixed step from piece
+  // to piece, and bit c of cmask says whether its 8 columns of chunk c lie in the row. The
+  // two base pointers are held in registers for the whole band (read once, not per piece).
+  uint32_t cmask = 0;
+  const uint16_t *gptr = t.g, *zptr = t.zeros;
+  if constexpr (VEC && !MOM) {
+    for (int c = 0; c < zcw; c++)
+      if ((int64_t)c * kChunk + lane * 8 < m) cmask |= 1u << c;
+    asm volatile("" : "+v"(gptr), "+v"(zptr));
+  }
+  const int64_t off_step = (int64_t)dr * ld + (int64_t)dc * kChunk;
+  const int64_t off_wrap = ld - (int64_t)zcw * kChunk;
   auto issue = [&](int64_t blk, unsigned char *buf, float *rbuf) {
     const int64_t rbase = r0 + blk * br;
     int r = pr0, c = pc0;
+    if constexpr (VEC && !MOM) {
+      int64_t off = (rbase + pr0) * ld + (int64_t)pc0 * kChunk + lane * 8;   // elements
+      for (int p = wave; p < npieces; p += kZWaves) {
+        const bool ok = rbase + r < r1 && ((cmask >> c) & 1u);
+        dma16(ok ? (const void *)(gptr + off) : (const void *)zptr, buf + (size_t)p * 1024);
+        r += dr;
+        c += dc;
+        off += off_step;
+        if (c >= zcw) {
+          c -= zcw;
+          r++;
+          off += off_wrap;
+        }
+      }
+    } else
     for (int p = wave; p < npieces; p += kZWaves) {
       const bool rok = rbase + r < r1;   // wave-uniform
       const int64_t i = rok ? rbase + r : r1 - 1;
@@ -654,25 +686,39 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         rbuf[lane] = ldg(t.R + ic);
     }
   };
-  // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows (up
-  // to eight 16-byte reads in flight together, one wait for them) into uk[b0 .. b0 + RBB).
-  // Staged padding is zero; a segment past the row's last chunk (wave-uniform) reads the
-  // zero area instead.
+  // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows into
+  // uk[b0 .. b0 + RBB). Staged padding is zero; a segment past the row's last chunk
+  // (wave-uniform) reads the buffer's zero area instead. Every address lies in the buffer
+  // being read, which the compiler can tell from the one the next block is loading into,
+  // so plain reads wait for the LDS alone (lgkmcnt), never for that load. The momentum
+  // variants keep one inline batch with its wait: plain reads there raise the registers
+  // the compiler holds (and spills).
   constexpr int RBB = (8 / NSEG < RB ? 8 / NSEG : RB) > 0 ? (8 / NSEG < RB ? 8 / NSEG : RB) : 1;
+  // the block's staged gradient stays in registers from the first sweep to the second where
+  // it fits (no momentum, up to two chunks per wave; the other variants would spill)
+  constexpr bool KEEP = !MOM && NSEG <= 2;
   auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&uk)[RB][NSEG]) {
     const unsigned char *ptr[RBB * NSEG];
 #pragma unroll
     for (int b = 0; b < RBB; b++)
 #pragma unroll
       for (int s = 0; s < NSEG; s++)
-        ptr[b * NSEG + s] = (chs[s] < zcw ? buf + (size_t)((grp_c * RB + b0 + b) * zcw + chs[s]) * 1024 : zlds) +
-                            lane * 16;
-    uint4 u[RBB * NSEG];
-    lds_read16_n<RBB * NSEG>(ptr, u);
+        ptr[b * NSEG + s] =
+            buf + (chs[s] < zcw ? (size_t)((grp_c * RB + b0 + b) * zcw + chs[s]) * 1024 : (size_t)kZLdsBytes) +
+            lane * 16;
+    if constexpr (KEEP) {
 #pragma unroll
-    for (int b = 0; b < RBB; b++)
+      for (int b = 0; b < RBB; b++)
 #pragma unroll
-      for (int s = 0; s < NSEG; s++) uk[b0 + b][s] = u[b * NSEG + s];
+        for (int s = 0; s < NSEG; s++) uk[b0 + b][s] = lds_read16(ptr[b * NSEG + s]);
+    } else {
+      uint4 u[RBB * NSEG];
+      lds_read16_n<RBB * NSEG>(ptr, u);
+#pragma unroll
+      for (int b = 0; b < RBB; b++)
+#pragma unroll
+        for (int s = 0; s < NSEG; s++) uk[b0 + b][s] = u[b * NSEG + s];
+    }
   };
   auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt) {
     __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
@@ -680,10 +726,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
     const int64_t rbase = r0 + blk * br;
     double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
-    // The lane's staged gradient of the block, read from LDS by the first sweep and kept in
-    // registers for the second where they fit (no momentum, up to two chunks per wave; the
-    // other variants would spill and read the block again)
-    constexpr bool KEEP = !MOM && NSEG <= 2;
+    // the lane's staged gradient of the block (the second sweep reads it again unless KEEP)
     uint4 uk[RB][NSEG];
     // row and column sums of g^2 (bf16 squares are exact in double); an idle wave's
     // accumulators are never used. Mode 2 has them from the first pass.
@@ -795,7 +838,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
           }
           if (MOM) {
             const unsigned char *mp =
-                (chs[s] < zcw ? cur + goff_m + (size_t)(r * zcw + chs[s]) * 2048 : zlds) + lane * 32;
+                cur + (chs[s] < zcw ? goff_m + (size_t)(r * zcw + chs[s]) * 2048 : (size_t)kZLdsBytes) + lane * 32;
             const unsigned char *mpp[2] = {mp, mp + 16};
             uint4 mv[2];
             lds_read16_n<2>(mpp, mv);
@@ -925,14 +968,15 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 template <int NSEG, bool MOM, bool VEC, bool GN>
 __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restrict__ TT,
                                                         const Item *__restrict__ items, StepConsts k, int mode_arg) {
-  __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes];
-  __shared__ __attribute__((aligned(16))) unsigned char bufB[kZLdsBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes + 2048];
+  __shared__ __attribute__((aligned(16))) unsigned char bufB[kZLdsBytes + 2048];
   __shared__ float rbA[64], rbB[64];
   __shared__ double rowsh[2 * kZRowSlots];
   __shared__ double sh[5 * kZWaves];
   __shared__ float rstash[kZMaxBandRows];
-  __shared__ __attribute__((aligned(16))) unsigned char zlds[2048];   // zeros: 32 bytes per lane
-  reinterpret_cast<uint32_t *>(zlds)[threadIdx.x] = 0u;   // complete before the first block's wait
+  // each buffer ends in a zero area of 32 bytes per lane, cleared before the first block's wait
+  reinterpret_cast<uint32_t *>(bufA + kZLdsBytes)[threadIdx.x] = 0u;
+  reinterpret_cast<uint32_t *>(bufB + kZLdsBytes)[threadIdx.x] = 0u;
   static_assert(kZThreads * 4 == 2048, "one word per thread");
   const int mode = GN ? mode_arg : 0;
   const Item it = items[blockIdx.x];
@@ -940,11 +984,11 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
   // and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG <= 2 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else
-    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash, zlds);
+    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
 }
 
 // Reductions of the clip stage, over the whole work-group (a tensor of its own) or over one

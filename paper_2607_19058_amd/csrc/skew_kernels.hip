@@ -554,7 +554,7 @@ __device__ __forceinline__ double rsq_d(double x) {
   return y * fma(-0.5 * x * y, y, 1.5);
 }
 
-template <int NSEG, int RB, bool MOM, bool VEC>
+template <int NSEG, int RB, bool MOM, bool VEC, bool GN>
 __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, int mode,
                                          unsigned char *bufA, unsigned char *bufB, float *rbA, float *rbB,
                                          double *rowsh, double *sh, float *rstash) {
@@ -615,24 +615,42 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   const int dr = kZWaves / zcw, dc = kZWaves - (kZWaves / zcw) * zcw;   // step of 8 pieces
   // Direct loads of the gradient alone: the lane's source moves by a fixed step from piece
   // to piece, and bit c of cmask says whether its 8 columns of chunk c lie in the row. The
-  // two base pointers are held in registers for the whole band (read once, not per piece).
-  uint32_t cmask = 0;
+  // base pointers are held in registers for the whole band (read once, not per piece).
+  // With momentum, the fp32 row of M follows in two 1 KiB halves per piece (masks cm0, cm1).
+  // (The momentum variants with four chunks per wave or the gradient-norm passes keep the
+  // general loop: the registers of the lean one would spill there.)
+  constexpr bool LEAN = VEC && (!MOM || (NSEG <= 2 && !GN));
+  uint32_t cmask = 0, cm0 = 0, cm1 = 0;
   const uint16_t *gptr = t.g, *zptr = t.zeros;
-  if constexpr (VEC && !MOM) {
-    for (int c = 0; c < zcw; c++)
+  const float *mptr = t.M, *rptr = t.R;
+  if constexpr (LEAN) {
+    for (int c = 0; c < zcw; c++) {
       if ((int64_t)c * kChunk + lane * 8 < m) cmask |= 1u << c;
-    asm volatile("" : "+v"(gptr), "+v"(zptr));
+      if ((int64_t)c * kChunk + lane * 4 < m) cm0 |= 1u << c;
+      if ((int64_t)c * kChunk + lane * 4 + 256 < m) cm1 |= 1u << c;
+    }
+    asm volatile("" : "+v"(gptr), "+v"(zptr), "+v"(rptr));
+    if constexpr (MOM) asm volatile("" : "+v"(mptr));
   }
   const int64_t off_step = (int64_t)dr * ld + (int64_t)dc * kChunk;
   const int64_t off_wrap = ld - (int64_t)zcw * kChunk;
   auto issue = [&](int64_t blk, unsigned char *buf, float *rbuf) {
     const int64_t rbase = r0 + blk * br;
     int r = pr0, c = pc0;
-    if constexpr (VEC && !MOM) {
-      int64_t off = (rbase + pr0) * ld + (int64_t)pc0 * kChunk + lane * 8;   // elements
+    if constexpr (LEAN) {
+      int64_t off = (rbase + pr0) * ld + (int64_t)pc0 * kChunk + lane * 8;   // elements of G
+      int64_t moff = (rbase + pr0) * m + (int64_t)pc0 * kChunk + lane * 4;   // elements of M
       for (int p = wave; p < npieces; p += kZWaves) {
-        const bool ok = rbase + r < r1 && ((cmask >> c) & 1u);
-        dma16(ok ? (const void *)(gptr + off) : (const void *)zptr, buf + (size_t)p * 1024);
+        const bool rok = rbase + r < r1;
+        dma16((rok && ((cmask >> c) & 1u)) ? (const void *)(gptr + off) : (const void *)zptr,
+              buf + (size_t)p * 1024);
+        if constexpr (MOM) {
+          dma16((rok && ((cm0 >> c) & 1u)) ? (const void *)(mptr + moff) : (const void *)zptr,
+                buf + goff_m + (size_t)p * 2048);
+          dma16((rok && ((cm1 >> c) & 1u)) ? (const void *)(mptr + moff + 256) : (const void *)zptr,
+                buf + goff_m + (size_t)p * 2048 + 1024);
+          moff += (int64_t)dr * m + (int64_t)dc * kChunk;
+        }
         r += dr;
         c += dc;
         off += off_step;
@@ -640,6 +658,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
           c -= zcw;
           r++;
           off += off_wrap;
+          if constexpr (MOM) moff += m - (int64_t)zcw * kChunk;
         }
       }
     } else
@@ -680,7 +699,9 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     if (wave == 0) {
       const int64_t i = rbase + (lane < br ? lane : br - 1);
       const int64_t ic = i < r1 ? i : r1 - 1;
-      if (VEC)
+      if (LEAN)
+        dma4(rptr + ic, rbuf);
+      else if (VEC)
         dma4(t.R + ic, rbuf);
       else
         rbuf[lane] = ldg(t.R + ic);
@@ -984,11 +1005,11 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
   // and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG <= 2 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else
-    p1z_body<NSEG, 1, MOM, VEC>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
 }
 
 // Reductions of the clip stage, over the whole work-group (a tensor of its own) or over one

@@ -112,3 +112,23 @@ def test_expert_rows_always_zero():
     log("[parity] experts with 90% zero rows, 19 tensors, 8 steps, all compared")
     st = run(wl)
     assert st.ok(), st
+
+
+@pytest.mark.parametrize("hp", [oracle.DEFAULTS, dict(oracle.DEFAULTS, weight_decay=0.05, max_grad_norm=1.0)],
+                         ids=["plain", "gnorm+decay"])
+def test_row_band_widths_with_partial_chunks(hp):
+    """Row-band matrices whose rows end inside a 512-column chunk, with and without momentum:
+    the block loads mask the lanes past the row (for M, each of its two 1 KiB halves on its
+    own) and the last block of a band holds rows past the band's end. Widths of 2, 4, 9 and
+    17 chunks take one to four chunks per wave (17: the general load loop); every tensor
+    compared."""
+    shapes = [("bb.w1000", W.BACKBONE, (300, 1000)), ("bb.w1544", W.BACKBONE, (70, 1544)),
+              ("bb.w4104", W.BACKBONE, (33, 4104)), ("bb.w8200", W.BACKBONE, (40, 8200)),
+              ("ex.w1544", W.EXPERT, (96, 1544)), ("ex.w8200", W.EXPERT, (24, 8200)),
+              ("rt", W.ROUTER, (256, 8))]
+    specs = [W.Spec(name, tier, shape, k) for k, (name, tier, shape) in enumerate(shapes)]
+    wl = W.Workload("partial_chunks", specs, 4)
+    log(f"[parity] {len(specs)} row-band widths with partial chunks, 4 steps, {hp}; all compared")
+    st = run(wl, hp=hp)
+    assert st.ok(), st
+    assert st.compared > 0

@@ -431,10 +431,10 @@ __device__ __forceinline__ void dma4(const void *g, void *lds) {
 constexpr int kWaitVmLgkm0 = 0x0070;
 constexpr int kWaitLgkm0 = 0xC07F;
 
-// Reads from a staging buffer are opaque to the compiler's wait insertion, which cannot
-// tell the buffer being read from the one the next block is loading into and would
-// otherwise wait for that load; the staged data is known to be complete from the wait
-// and barrier that open each block. N reads are in flight together, then one wait.
+// Inline reads of a staging buffer (the momentum variants, where plain loads would raise
+// their registers): opaque to the compiler's wait insertion, so no wait for the block
+// loading into the other buffer is added; the staged data is known to be complete from the
+// wait and barrier that open each block. N reads are in flight together, then one wait.
 __device__ __forceinline__ uint32_t lds_addr(const unsigned char *p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char *)p;
 }

@@ -613,12 +613,12 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // stages the block's old R values.
   const int pr0 = wave / zcw, pc0 = wave - pr0 * zcw;                   // piece `wave`: (row, chunk)
   const int dr = kZWaves / zcw, dc = kZWaves - (kZWaves / zcw) * zcw;   // step of 8 pieces
-  // Direct loads of the gradient alone: the lane's source moves by a fixed step from piece
-  // to piece, and bit c of cmask says whether its 8 columns of chunk c lie in the row. The
-  // base pointers are held in registers for the whole band (read once, not per piece).
-  // With momentum, the fp32 row of M follows in two 1 KiB halves per piece (masks cm0, cm1).
-  // (The momentum variants with four chunks per wave or the gradient-norm passes keep the
-  // general loop: the registers of the lean one would spill there.)
+  // Direct loads (the lean loop): the lane's source moves by a fixed step from piece to
+  // piece, and bit c of cmask says whether its 8 columns of chunk c lie in the row (zcw <= 32:
+  // at most 8 waves of 4 chunks). The base pointers are held in registers for the whole band
+  // (read once, not per piece). With momentum, the fp32 row of M follows in two 1 KiB halves
+  // per piece (masks cm0, cm1). The momentum variants with four chunks per wave or in the
+  // gradient-norm passes keep the general loop: the registers of the lean one would spill.
   constexpr bool LEAN = VEC && (!MOM || (NSEG <= 2 && !GN));
   uint32_t cmask = 0, cm0 = 0, cm1 = 0;
   const uint16_t *gptr = t.g, *zptr = t.zeros;

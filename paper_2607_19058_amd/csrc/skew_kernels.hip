@@ -48,10 +48,6 @@ __device__ __forceinline__ float4 ldg(const float4 *p) {
   const f32x4_t v = ldg(reinterpret_cast<const f32x4_t *>(p));
   return make_float4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ void stg(uint4 *p, uint4 v) {
-  const u32x4_t u = {v.x, v.y, v.z, v.w};
-  stg(reinterpret_cast<u32x4_t *>(p), u);
-}
 __device__ __forceinline__ void stg(float4 *p, float4 v) {
   const f32x4_t u = {v.x, v.y, v.z, v.w};
   stg(reinterpret_cast<f32x4_t *>(p), u);

@@ -21,10 +21,8 @@
  *    "host" pointers are ordinary host memory. The caller owns all of them.
  *  - Streams are hipStream_t values passed as void* (NULL = the default stream).
  *    skew_state_init and skew_step are stream-ordered and never synchronise the
- *    device, except skew_state_init, which waits for its own table upload. A context
- *    may own one more stream of default priority: skew_step forks part of its work onto
- *    it with events and joins it back into the caller's stream before the step's end,
- *    so work queued on the caller's stream after skew_step sees the whole step.
+ *    device, except skew_state_init, which waits for its own table upload. Every
+ *    kernel of a step runs on the caller's stream.
  *  - bf16 is IEEE binary32 truncated to its upper 16 bits (the bfloat16 format).
  *  - Sizes and element indices are 64-bit throughout (tensors of >= 2^31 elements).
  */

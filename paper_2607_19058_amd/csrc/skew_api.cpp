@@ -20,12 +20,10 @@ const char *const kLaunchNames[kLaunches] = {"p1z_rowband_stats", "p1z_rowband_s
                                              "grad_norm"};
 }  // namespace
 
-// an item list with the bounds of each pipeline group in it
-struct GroupedList {
-  Item *d = nullptr;
-  std::vector<int64_t> bound;   // group g: items [bound[g], bound[g + 1])
-  int64_t count(int g) const { return bound[g + 1] - bound[g]; }
-  const Item *at(int g) const { return d + bound[g]; }
+// a contiguous list of work items in the workspace
+struct ItemList {
+  const Item *d = nullptr;
+  int64_t n = 0;
 };
 
 struct skew_ctx {
@@ -33,15 +31,10 @@ struct skew_ctx {
   char *ws = nullptr;   // workspace base (device)
   DevTensor *d_table = nullptr;
   RecheckLists *lists = nullptr;
-  GroupedList p1, fold, p2, p3, clip, fold_rows;
-  GroupedList fold_z, fold_w;   // the fold's items of row-band tensors and of the others
+  ItemList p1, fold, p2, p3, clip, fold_rows;
   float *gscale = nullptr;   // device: the gradient-norm mode's scale
   double *gsq = nullptr;     // device: per-tensor sums of g^2
-  GroupedList z[kZVariants];   // row-band pass items, one list per kernel variant
-  hipStream_t side = nullptr;  // the update pass of the pipeline runs here
-  // [0]: step start, [1]: update pass done, [2 + g]: group g ready, [2 + ngroups]: the side
-  // stream's statistics of wide and exact tensors done
-  std::vector<hipEvent_t> sync;
+  ItemList z[kZVariants];    // row-band pass items, one list per kernel variant
   // diagnostics: per recorded step, (launch kind, start event, end event) of every launch
   struct Timed {
     int kind;
@@ -53,8 +46,6 @@ struct skew_ctx {
   size_t ev_next = 0;
   ~skew_ctx() {
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
-    for (hipEvent_t e : sync) (void)hipEventDestroy(e);
-    if (side) (void)hipStreamDestroy(side);
   }
 };
 
@@ -126,21 +117,22 @@ int skew_state_bytes(const skew_tensor_desc *d, int n, size_t *state_bytes, size
   return SKEW_OK;
 }
 
-int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes, void *workspace,
-                    size_t workspace_bytes, void *stream) {
-  if (ctx == nullptr) return SKEW_EINVAL;
-  *ctx = nullptr;
-  Plan p;
-  int rc = plan_build(d, n, &p);
-  if (rc != SKEW_OK) return rc;
-  if (state_bytes < p.state_bytes || workspace_bytes < p.ws_bytes) return SKEW_ENOSPACE;
-  if ((p.state_bytes > 0 && state == nullptr) || workspace == nullptr) return SKEW_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// Context set-up on a planned table with the workspace `ws` of ws_bytes: fills the state
+// pointers of d, zero-fills state and workspace on `stream` and uploads the device table
+// and item lists (waiting for the upload: the host staging vectors die on return).
+int init_ctx(skew_ctx **ctx, Plan &p, skew_tensor_desc *d, int n, void *state, size_t state_bytes, char *ws,
+             size_t ws_bytes, hipStream_t s) {
+  if (state_bytes < p.state_bytes || ws_bytes < p.ws_bytes) return SKEW_ENOSPACE;
+  if ((p.state_bytes > 0 && state == nullptr) || ws == nullptr) return SKEW_EINVAL;
   const int nt = (int)p.t.size();   // sub-tensors (a stacked tensor's slices are several)
   for (int i = 0; i < nt; i++)
     if (!p.t[i].empty && (d[p.t[i].desc].w == nullptr || d[p.t[i].desc].g == nullptr)) return SKEW_EINVAL;
 
   char *st = static_cast<char *>(state);
-  char *ws = static_cast<char *>(workspace);
   auto sp = [&](size_t off) { return off == SIZE_MAX ? nullptr : reinterpret_cast<float *>(st + off); };
   for (int di = 0; di < n; di++) {   // the caller's view: each descriptor's state from its first slice
     const TensorPlan &tp = p.t[(size_t)p.desc_sub0[(size_t)di]];
@@ -203,8 +195,7 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
     x.tensor_id = dd.tensor_id;
   }
   // row-band pass items by kernel variant (16-byte aligned rows or element loads is known
-  // only here, from the pointers); every list keeps tensor order, so each pipeline group
-  // is a contiguous range of it
+  // only here, from the pointers)
   std::vector<Item> zv[kZVariants];
   for (const Item &it : p.z) {
     const DevTensor &x = table[it.tensor];
@@ -219,11 +210,9 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   std::vector<Item> items;
   items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() +
                 p.fold_rows.size() + 1);
-  auto add = [&](GroupedList &gl, const std::vector<Item> &v) {
-    gl.d = base + items.size();
-    gl.bound.assign((size_t)p.ngroups + 1, 0);
-    for (const Item &it : v) gl.bound[(size_t)p.tgroup[it.tensor] + 1]++;
-    for (int g = 0; g < p.ngroups; g++) gl.bound[g + 1] += gl.bound[g];
+  auto add = [&](ItemList &l, const std::vector<Item> &v) {
+    l.d = base + items.size();
+    l.n = (int64_t)v.size();
     items.insert(items.end(), v.begin(), v.end());
   };
   add(c->p1, p.p1);
@@ -233,12 +222,6 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   add(c->p3, p.p3);
   add(c->clip, p.clip);
   add(c->fold_rows, p.fold_rows);
-  {
-    std::vector<Item> fz, fw;
-    for (const Item &it : p.fold) (table[it.tensor].zpath ? fz : fw).push_back(it);
-    add(c->fold_z, fz);
-    add(c->fold_w, fw);
-  }
   if (items.empty()) items.push_back({0, 0});
   if (sizeof(Item) * items.size() > p.off_lists - p.off_items) {   // the planner's region must hold them
     delete c;
@@ -247,24 +230,15 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   c->gscale = reinterpret_cast<float *>(ws + p.off_gscale);
   c->gsq = reinterpret_cast<double *>(ws + p.off_gsq);
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  // the side stream (it takes a hardware queue) runs the update pass of a pipeline of several
-  // groups, or the statistics of wide and exact tensors beside the row-band pass
-  const bool side = p.ngroups > 1 || !p.p1.empty() || !p.p2.empty();
-  hipError_t e = side ? hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) : hipSuccess;
-  for (int i = 0; e == hipSuccess && i < p.ngroups + 3; i++) {
-    hipEvent_t ev;
-    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-    if (e == hipSuccess) c->sync.push_back(ev);
-  }
   // zero state and workspace (the per-tensor scalars start with no regime prediction)
-  if (e == hipSuccess && p.state_bytes > 0) e = hipMemsetAsync(state, 0, p.state_bytes, s);
+  hipError_t e = hipSuccess;
+  if (p.state_bytes > 0) e = hipMemsetAsync(state, 0, p.state_bytes, s);
   if (e == hipSuccess) e = hipMemsetAsync(ws, 0, p.ws_bytes, s);
   if (e == hipSuccess)
     e = hipMemcpyAsync(c->d_table, table.data(), sizeof(DevTensor) * table.size(), hipMemcpyHostToDevice, s);
   if (e == hipSuccess)
     e = hipMemcpyAsync(base, items.data(), sizeof(Item) * items.size(), hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);  // the host staging vectors die on return
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
     delete c;
     return SKEW_EHIP;
@@ -275,10 +249,19 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
   return SKEW_OK;
 }
 
-// the re-check lists of tensor group g
-static RecheckLists *group_lists(skew_ctx *ctx, int g) {
-  return reinterpret_cast<RecheckLists *>(reinterpret_cast<unsigned char *>(ctx->lists) +
-                                          (size_t)g * ctx->plan.lists_stride);
+}  // namespace
+
+extern "C" {
+
+int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes, void *workspace,
+                    size_t workspace_bytes, void *stream) {
+  if (ctx == nullptr) return SKEW_EINVAL;
+  *ctx = nullptr;
+  Plan p;
+  const int rc = plan_build(d, n, &p);
+  if (rc != SKEW_OK) return rc;
+  return init_ctx(ctx, p, d, n, state, state_bytes, static_cast<char *>(workspace), workspace_bytes,
+                  static_cast<hipStream_t>(stream));
 }
 
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
@@ -287,107 +270,61 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   k.gscale = ctx->gscale;
   k.gsq = ctx->gsq;
   const Plan &p = ctx->plan;
-  if (k.gclip && p.ngroups != 1) return SKEW_EINVAL;   // the global norm couples every tensor
-  hipStream_t s0 = static_cast<hipStream_t>(stream), s1 = ctx->side;
+  hipStream_t s = static_cast<hipStream_t>(stream);
   std::vector<skew_ctx::Timed> *rec = nullptr;
   if (ctx->ev_used < ctx->ev_steps) {
     rec = &ctx->timed[(size_t)ctx->ev_used++];
     rec->clear();
   }
   int e = 0;
-  // one launch of kind j on stream st, bracketed by timing events when recording
-  auto run = [&](int j, hipStream_t st, auto &&launch) {
+  // one launch of kind j, bracketed by timing events when recording
+  auto run = [&](int j, auto &&launch) {
     if (e != 0) return;
     if (rec && ctx->ev_next + 2 <= ctx->ev_pool.size()) {
       skew_ctx::Timed t{j, ctx->ev_pool[ctx->ev_next], ctx->ev_pool[ctx->ev_next + 1]};
       ctx->ev_next += 2;
-      e = (int)hipEventRecord(t.a, st);
+      e = (int)hipEventRecord(t.a, s);
       if (e == 0) e = launch();
-      if (e == 0) e = (int)hipEventRecord(t.b, st);
+      if (e == 0) e = (int)hipEventRecord(t.b, s);
       rec->push_back(t);
     } else {
       e = launch();
     }
   };
   const DevTensor *T = ctx->d_table;
-  // the side stream starts after everything the caller queued before the step
-  if (p.ngroups > 1) {
-    e = (int)hipEventRecord(ctx->sync[0], s0);
-    if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[0], 0);
-  }
   const int nt = (int)p.t.size();
-  for (int g = 0; g < p.ngroups && e == 0; g++) {
-    // pass 1, fold and clip stage of group g on the caller's stream
-    bool p2_done = false;
-    if (!k.gclip && p.ngroups == 1 && s1 != nullptr) {
-      // the wide tensors' pass 1 and fold and the update sums of wide and exact tensors
-      // run on the side stream, beside the row-band pass (which leaves ALU time and
-      // registers free); the clip stage waits for both
-      e = (int)hipEventRecord(ctx->sync[0], s0);
-      if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[0], 0);
-      if (ctx->p1.count(g) > 0) run(2, s1, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s1); });
-      if (ctx->fold_w.count(g) > 0)
-        run(3, s1, [&] { return launch_fold(T, ctx->fold_w.at(g), ctx->fold_w.count(g), k, 0, s1); });
-      if (ctx->p2.count(g) > 0) run(4, s1, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s1); });
-      if (e == 0) e = (int)hipEventRecord(ctx->sync[2 + p.ngroups], s1);
-      for (int v = 0; v < kZVariants; v++)
-        if (ctx->z[v].count(g) > 0)
-          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 0, s0); });
-      if (ctx->fold_z.count(g) > 0)
-        run(3, s0, [&] { return launch_fold(T, ctx->fold_z.at(g), ctx->fold_z.count(g), k, 0, s0); });
-      if (e == 0) e = (int)hipStreamWaitEvent(s0, ctx->sync[2 + p.ngroups], 0);
-      p2_done = true;
-    } else if (!k.gclip) {
-      for (int v = 0; v < kZVariants; v++)
-        if (ctx->z[v].count(g) > 0)
-          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 0, s0); });
-      if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
-      if (ctx->fold.count(g) > 0)
-        run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, 0, s0); });
-    } else {
-      // gradient-norm mode (one group): the scale needs every tensor's sum of g^2 before
-      // any statistic, so the row-band pass runs twice: sums, then z with R folded
-      for (int v = 0; v < kZVariants; v++)
-        if (ctx->z[v].count(g) > 0)
-          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 1, s0); });
-      if (ctx->p1.count(g) > 0) run(2, s0, [&] { return launch_p1(T, ctx->p1.at(g), ctx->p1.count(g), s0); });
-      if (ctx->p2.count(g) > 0) run(9, s0, [&] { return launch_gsq(T, ctx->p2.at(g), ctx->p2.count(g), s0); });
-      run(9, s0, [&] { return launch_gnorm(T, nt, k, s0); });
-      if (ctx->fold_rows.count(g) > 0)
-        run(3, s0, [&] { return launch_fold(T, ctx->fold_rows.at(g), ctx->fold_rows.count(g), k, 1, s0); });
-      for (int v = 0; v < kZVariants; v++)
-        if (ctx->z[v].count(g) > 0)
-          run(v & 1, s0, [&] { return launch_p1z(T, ctx->z[v].at(g), ctx->z[v].count(g), k, v, 2, s0); });
-      if (ctx->fold.count(g) > 0)
-        run(3, s0, [&] { return launch_fold(T, ctx->fold.at(g), ctx->fold.count(g), k, 2, s0); });
-    }
-    if (!p2_done && ctx->p2.count(g) > 0)
-      run(4, s0, [&] { return launch_p2(T, ctx->p2.at(g), ctx->p2.count(g), k, s0); });
-    if (ctx->clip.count(g) > 0) {
-      RecheckLists *L = group_lists(ctx, g);
-      run(5, s0, [&] { return launch_clip(T, ctx->clip.at(g), ctx->clip.count(g), k, L, nt, s0); });
-      // re-checks of the tensors the clip stage listed (launches with empty lists exit at once)
-      run(6, s0, [&] { return launch_recheck(T, L, nt, k, 1, s0); });
-      run(7, s0, [&] { return launch_clip_recheck(T, L, nt, k, 1, s0); });
-      run(6, s0, [&] { return launch_recheck(T, L, nt, k, 2, s0); });
-      run(7, s0, [&] { return launch_clip_recheck(T, L, nt, k, 2, s0); });
-    }
-    if (p.ngroups == 1) {
-      if (ctx->p3.count(g) > 0)
-        run(8, s0, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, group_lists(ctx, g), s0); });
-      continue;
-    }
-    if (e == 0) e = (int)hipEventRecord(ctx->sync[2 + g], s0);
-    // the update pass of group g on the side stream, concurrent with pass 1 of group g + 1
-    if (e == 0) e = (int)hipStreamWaitEvent(s1, ctx->sync[2 + g], 0);
-    if (ctx->p3.count(g) > 0)
-      run(8, s1, [&] { return launch_p3(T, ctx->p3.at(g), ctx->p3.count(g), k, group_lists(ctx, g), s1); });
+  RecheckLists *L = ctx->lists;
+  auto rowband = [&](int mode) {
+    for (int v = 0; v < kZVariants; v++)
+      if (ctx->z[v].n > 0) run(v & 1, [&] { return launch_p1z(T, ctx->z[v].d, ctx->z[v].n, k, v, mode, s); });
+  };
+  if (!k.gclip) {
+    // statistics: the row-band pass, pass 1 of wide factored tensors, the fold
+    rowband(0);
+    if (ctx->p1.n > 0) run(2, [&] { return launch_p1(T, ctx->p1.d, ctx->p1.n, s); });
+    if (ctx->fold.n > 0) run(3, [&] { return launch_fold(T, ctx->fold.d, ctx->fold.n, k, 0, s); });
+  } else {
+    // gradient-norm mode: the scale needs every tensor's sum of g^2 before any statistic,
+    // so the row-band pass runs twice: sums, then z with R folded
+    rowband(1);
+    if (ctx->p1.n > 0) run(2, [&] { return launch_p1(T, ctx->p1.d, ctx->p1.n, s); });
+    if (ctx->p2.n > 0) run(9, [&] { return launch_gsq(T, ctx->p2.d, ctx->p2.n, s); });
+    run(9, [&] { return launch_gnorm(T, nt, k, s); });
+    if (ctx->fold_rows.n > 0) run(3, [&] { return launch_fold(T, ctx->fold_rows.d, ctx->fold_rows.n, k, 1, s); });
+    rowband(2);
+    if (ctx->fold.n > 0) run(3, [&] { return launch_fold(T, ctx->fold.d, ctx->fold.n, k, 2, s); });
   }
-  // the caller's stream continues after the last update
-  if (e == 0 && p.ngroups > 1) {
-    e = (int)hipEventRecord(ctx->sync[1], s1);
-    if (e == 0) e = (int)hipStreamWaitEvent(s0, ctx->sync[1], 0);
+  // update sums of wide and exact tensors, the clip stage and its re-checks (launches with
+  // empty lists exit at once), then the update
+  if (ctx->p2.n > 0) run(4, [&] { return launch_p2(T, ctx->p2.d, ctx->p2.n, k, s); });
+  if (ctx->clip.n > 0) {
+    run(5, [&] { return launch_clip(T, ctx->clip.d, ctx->clip.n, k, L, nt, s); });
+    run(6, [&] { return launch_recheck(T, L, nt, k, 1, s); });
+    run(7, [&] { return launch_clip_recheck(T, L, nt, k, 1, s); });
+    run(6, [&] { return launch_recheck(T, L, nt, k, 2, s); });
+    run(7, [&] { return launch_clip_recheck(T, L, nt, k, 2, s); });
   }
+  if (ctx->p3.n > 0) run(8, [&] { return launch_p3(T, ctx->p3.d, ctx->p3.n, k, L, s); });
   return e == 0 ? SKEW_OK : SKEW_EHIP;
 }
 
@@ -398,8 +335,8 @@ int skew_timing_enable(skew_ctx *ctx, int max_steps) {
   ctx->timed.clear();
   ctx->ev_steps = ctx->ev_used = 0;
   ctx->ev_next = 0;
-  // at most one launch of each kind per group and step (the row-band variants share two kinds)
-  const size_t per_step = (size_t)ctx->plan.ngroups * (kLaunches + 2 * kZVariants + 8) * 2;
+  // at most one launch of each kind per step (the row-band variants share two kinds)
+  const size_t per_step = (size_t)(kLaunches + 2 * kZVariants + 8) * 2;
   const size_t n = (size_t)max_steps * per_step;
   ctx->ev_pool.reserve(n);
   for (size_t i = 0; i < n; i++) {

@@ -43,8 +43,6 @@ struct TensorScalars {
 // Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
 // launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for
 // the exact float sequence. Counts are zeroed by the update pass at the end of each step.
-// Each group of tensors has its own lists (its update pass may run beside the next
-// group's clip stage).
 struct RecheckLists {
   int32_t n1, n2;
   int32_t pad[62];
@@ -175,18 +173,10 @@ struct TensorPlan {
   int64_t zrows = 0;
 };
 
-// The step can run as a two-stream pipeline over groups of consecutive tensors (about
-// equal algorithmic bytes): the update pass (p3) of group g on one stream while pass 1,
-// the fold and the clip stage of group g + 1 run on the other. Measured on the 6.78B
-// workload, the two passes slow each other down more than they overlap (the row-band
-// pass needs whole CUs), so one group is used: every launch covers all tensors.
-constexpr int kMaxGroups = 1;
-
 struct Plan {
   std::vector<TensorPlan> t;                  // sub-tensors (the device table's entries)
   std::vector<int32_t> desc_sub0, desc_nsub;  // per descriptor: its first sub-tensor and their count
-  size_t off_lists = 0;                       // workspace offset of the first group's RecheckLists
-  size_t lists_stride = 0;                    // bytes from one group's RecheckLists to the next
+  size_t off_lists = 0;                       // workspace offset of the RecheckLists
   size_t off_zero = 0;                        // workspace offset of 256 zero bytes
   size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)
   size_t off_gsq = 0;                         // workspace offset of the per-tensor sums of g^2
@@ -195,8 +185,6 @@ struct Plan {
   // tensor (row-band tensors: rows [0, ceil(n / kFold)), then columns)
   std::vector<Item> fold_rows;
   std::vector<Item> z;                        // row-band pass items (split by kernel variant at init)
-  int32_t ngroups = 1;
-  std::vector<int32_t> tgroup;                // group of each tensor (item lists are in tensor order)
   size_t state_bytes = 0;
   size_t ws_bytes = 0;
   size_t off_table = 0, off_items = 0;   // workspace offsets of the device table and item lists

@@ -206,42 +206,16 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   }
   }
   const int nt = (int)p.t.size();   // sub-tensors: the device table's entries
-  // pipeline groups: consecutive tensors, about equal algorithmic bytes (gradient, weight
-  // read and write, and the state each tier reads and writes)
-  {
-    std::vector<double> bytes(nt, 0.0);
-    double total = 0.0;
-    int nonempty = 0;
-    for (int i = 0; i < nt; i++) {
-      const TensorPlan &tp = p.t[i];
-      if (tp.empty) continue;
-      bytes[i] = (double)tp.N * (6.0 + (tp.momentum ? 8.0 : 0.0) + (tp.kind == kExact ? 8.0 : 0.0));
-      total += bytes[i];
-      nonempty++;
-    }
-    p.ngroups = std::max(1, std::min(kMaxGroups, nonempty));
-    p.tgroup.assign(nt, 0);
-    double acc = 0.0;
-    for (int i = 0; i < nt; i++) {
-      const int g = total > 0.0 ? (int)(acc / total * p.ngroups) : 0;
-      p.tgroup[i] = std::min(g, p.ngroups - 1);
-      acc += bytes[i];
-    }
-  }
-  // update-pass and update-sum items: within each group, tiles that take longest go first,
-  // so that they do not finish last: the exact second moment's element-by-element path,
-  // and matrices narrower than a 512-column strip (idle lanes)
+  // update-pass and update-sum items: tiles that take longest go first, so that they do not
+  // finish last: the exact second moment's element-by-element path, and matrices narrower
+  // than a 512-column strip (idle lanes)
   {
     auto slow = [&](const Item &it) {
       const TensorPlan &tp = p.t[(size_t)it.tensor];
       return tp.kind == kExact || tp.m < 512;
     };
     auto order = [&](std::vector<Item> &v) {
-      std::stable_sort(v.begin(), v.end(), [&](const Item &a, const Item &b) {
-        const int ga = p.tgroup[(size_t)a.tensor], gb = p.tgroup[(size_t)b.tensor];
-        if (ga != gb) return ga < gb;
-        return slow(a) && !slow(b);
-      });
+      std::stable_sort(v.begin(), v.end(), [&](const Item &a, const Item &b) { return slow(a) && !slow(b); });
     };
     order(p.p3);
     order(p.p2);
@@ -256,8 +230,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + 2 * p.fold.size() + p.p2.size() + p.p3.size() +
                                      p.clip.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
-  p.lists_stride = align_up(sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
-  ws += p.lists_stride * (size_t)p.ngroups;
+  ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
   p.off_zero = ws;   // zero-filled with the workspace at set-up and never written
   ws = align_up(ws + 256);
   p.off_gscale = ws;

@@ -137,7 +137,11 @@ def _desc_for(tier: int, w, g, tensor_id: int, state_flags: int = 0) -> TensorDe
         if m > 1 and w.stride(2) != 1:
             raise ValueError("stacked matrices must be row-major (unit column stride)")
         ld = w.stride(1) if n > 1 else max(1, m)
-        ld = max(ld, m, 1)
+        if n > 1 and m > 0 and ld < m:
+            # rows that overlap (an expanded or unfolded view): the kernels write rows * ld
+            # elements in place, so such a view is refused rather than widened
+            raise ValueError(f"row stride {ld} is smaller than the row length {m} (overlapping rows)")
+        ld = max(ld, 1)
         if E > 1 and n * m > 0 and w.stride(0) != n * ld:   # (a tensor with no elements has no layout)
             raise ValueError("stacked slices must follow each other (slice stride rows * ld)")
         return make_desc(tier, 3, n, m, ld, tensor_id, w.data_ptr(), g.data_ptr(), batch=E,
@@ -148,7 +152,9 @@ def _desc_for(tier: int, w, g, tensor_id: int, state_flags: int = 0) -> TensorDe
     if m > 1 and w.stride(1) != 1:
         raise ValueError("matrices must be row-major (unit column stride)")
     ld = w.stride(0) if n > 1 else max(1, m)
-    return make_desc(tier, 2, n, m, max(ld, m, 1), tensor_id, w.data_ptr(), g.data_ptr(), state_flags=state_flags)
+    if n > 1 and m > 0 and ld < m:
+        raise ValueError(f"row stride {ld} is smaller than the row length {m} (overlapping rows)")
+    return make_desc(tier, 2, n, m, max(ld, 1), tensor_id, w.data_ptr(), g.data_ptr(), state_flags=state_flags)
 
 
 class SkewAdam:

@@ -132,3 +132,35 @@ def test_row_band_widths_with_partial_chunks(hp):
     st = run(wl, hp=hp)
     assert st.ok(), st
     assert st.compared > 0
+
+
+def test_overlapping_row_views_are_refused_before_any_launch():
+    """A view whose rows overlap (an expanded row, or an unfold window: row stride below the
+    row length) would make the in-place update write past the view; the binding refuses it
+    and the C ABI refuses a stride below the width as well."""
+    from paper_2607_19058_amd import TensorDesc, lib, make_desc
+    import ctypes
+    dev = torch.device("cuda")
+    base = torch.zeros((1, 1024), dtype=torch.bfloat16, device=dev)
+    w = base.expand(256, 1024)
+    g = torch.zeros((1, 1024), dtype=torch.bfloat16, device=dev).expand(256, 1024)
+    for tier in (W.BACKBONE, W.EXPERT, W.ROUTER):
+        with pytest.raises(ValueError, match="overlapping rows"):
+            SkewAdam([(tier, w, g, 0)])
+    flat = torch.zeros(4096, dtype=torch.bfloat16, device=dev)
+    win = flat.unfold(0, 1024, 512)          # rows of 1024 at a stride of 512
+    gwin = torch.zeros_like(flat).unfold(0, 1024, 512)
+    with pytest.raises(ValueError, match="overlapping rows"):
+        SkewAdam([(W.EXPERT, win, gwin, 0)])
+    stk = torch.zeros((1, 1, 1024), dtype=torch.bfloat16, device=dev).expand(2, 64, 1024)
+    with pytest.raises(ValueError, match="overlapping rows"):
+        SkewAdam([(W.EXPERT, stk, stk, 0)])
+    d = make_desc(W.EXPERT, 2, 256, 1024, 512, 0, base.data_ptr(), base.data_ptr())
+    arr = (TensorDesc * 1)(d)
+    ctx = ctypes.c_void_p()
+    st = torch.empty(1 << 20, dtype=torch.uint8, device=dev)
+    assert lib().skew_state_init(ctypes.byref(ctx), arr, 1, st.data_ptr(), st.numel(), st.data_ptr(), st.numel(),
+                                 None) == -1
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(base) == 0
+

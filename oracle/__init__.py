@@ -61,7 +61,7 @@ class _HParams(ctypes.Structure):
         ("eps", ctypes.c_float), ("clip_threshold", ctypes.c_float),
         ("step", ctypes.c_int64), ("seed", ctypes.c_uint64),
         ("weight_decay", ctypes.c_float), ("max_grad_norm", ctypes.c_float), ("gsq_total", ctypes.c_double),
-        ("exact_ulp", ctypes.c_int32),
+        ("exact_ulp", ctypes.c_int32), ("rbar_min_only", ctypes.c_int32),
     ]
 
 
@@ -159,14 +159,16 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
          beta1: float = DEFAULTS["beta1"], beta2: float = DEFAULTS["beta2"], eps: float = DEFAULTS["eps"],
          clip_threshold: float = DEFAULTS["clip_threshold"], want_u: bool = False, want_x: bool = False,
          want_y: bool = False, weight_decay: float = 0.0, max_grad_norm: float = 0.0,
-         gsq_total: Optional[float] = None, exact_ulp: bool = False) -> int:
+         gsq_total: Optional[float] = None, exact_ulp: bool = False, rbar_min_only: bool = False) -> int:
     """Run one oracle step over ``tensors`` in place. Returns the C status.
 
     weight_decay: lambda of the decoupled decay (router tier exempt). max_grad_norm > 0
     scales every gradient by min(1, max_grad_norm / (||G|| + 1e-6)) over all the tensors
     given, or over a larger set whose sum of squares is ``gsq_total``. The scale used is
     returned by ``last_gcoef()``. exact_ulp: the dither spans the exact bf16 ulp of w.
-    Tensors with STATE_FP32 hold float32 w and g (the arrays' dtype) and skip the cast."""
+    Tensors with STATE_FP32 hold float32 w and g (the arrays' dtype) and skip the cast.
+    rbar_min_only: the other reading of Alg. 1's eps-clamps (mean(R) guarded at FLT_MIN
+    instead of clamped at eps), for the sensitivity check of that reading only."""
     tensors = list(tensors)
     arr = (_Tensor * max(1, len(tensors)))()
     rms = np.full(max(1, len(tensors)), np.nan, np.float64)
@@ -198,7 +200,8 @@ def step(tensors: Iterable[Tensor], step: int, seed: int = 0, lr: float = DEFAUL
                          rms.ctypes.data + 8 * k, E if t.ndim == 3 else 0, int(t.state_flags))
         keep.append(t)
     hp = _HParams(lr, beta1, beta2, eps, clip_threshold, int(step), int(seed) & (2**64 - 1),
-                  weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total), int(exact_ulp))
+                  weight_decay, max_grad_norm, -1.0 if gsq_total is None else float(gsq_total), int(exact_ulp),
+                  int(rbar_min_only))
     gc = ctypes.c_float(0.0)
     rc = lib().skew_oracle_step_gcoef(ctypes.byref(hp), arr, len(tensors), ctypes.byref(gc))
     global _LAST_GCOEF

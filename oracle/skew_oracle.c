@@ -36,6 +36,7 @@
  * the dither's element index and N run over the whole tensor.
  */
 #include "skew_oracle.h"
+#include <float.h>
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -54,6 +55,7 @@ typedef struct {
   float gcoef;    /* the gradient scale c (1 when off) */
   double gc2;     /* c * c, exact in double */
   int exact_ulp;  /* dither width from the exact bf16 ulp of w */
+  int rbar_min_only;  /* mean(R) guarded at FLT_MIN only (the other reading of the eps-clamps) */
 } consts_t;
 
 /* a gradient or weight element: bf16 bits, or float32 for float32 masters */
@@ -179,7 +181,7 @@ static void factored_stats(const consts_t *K, const uint16_t *g, float *R, float
   double sr = 0.0;
   for (int64_t i = 0; i < n; i++) sr += (double)R[i];
   float rbar = (float)(sr / (double)n);
-  float q = max_nan(rbar, K->eps);
+  float q = max_nan(rbar, K->rbar_min_only ? FLT_MIN : K->eps);
   for (int64_t j = 0; j < m; j++) cprime[j] = C[j] / q;
 }
 
@@ -299,6 +301,7 @@ int skew_oracle_step_gcoef(const skew_oracle_hparams *hp, skew_oracle_tensor *t,
   K.seed = hp->seed;
   K.wd = (float)((double)hp->lr * (double)hp->weight_decay);
   K.exact_ulp = hp->exact_ulp != 0;
+  K.rbar_min_only = hp->rbar_min_only != 0;
   K.gclip = hp->max_grad_norm > 0.0f;
   K.gcoef = 1.0f;
   if (K.gclip) {

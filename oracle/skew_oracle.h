@@ -58,6 +58,11 @@ typedef struct {
                            (a step over a sample of a larger set passes the set's sum) */
   int32_t exact_ulp;    /* 1: the dither spans the exact bf16 ulp of w, xi ~ U(+-ulp(w)/2), in
                            place of the approximation ulp(w) ~ 2^-7 |w| (Sec. 3) */
+  int32_t rbar_min_only; /* 1: the other reading of Alg. 1's "eps-clamps" of the factored
+                           reconstruction, for a sensitivity check only: mean(R) is guarded
+                           at FLT_MIN (against 0/0) instead of being clamped at eps; the
+                           clamp max(R_i c'_j, eps) stays. 0: the reading both the oracle and
+                           the GPU library take (mean(R) clamped at eps). */
 } skew_oracle_hparams;
 
 /* One step over n tensors. Returns 0, -1 when step < 1, -2 when a tensor asks for float32

@@ -391,3 +391,29 @@ def test_fp32_master_router_matrix_and_factored_refusal():
     F = oracle.Tensor(tier=E, w=np.zeros((8, 4), np.float32), g=np.zeros((8, 4), np.float32), tensor_id=4,
                       state_flags=oracle.STATE_FP32).init_state()
     assert oracle.step([F], 1) == -2
+
+
+def test_exact_ulp_of_subnormal_weights():
+    """bf16 subnormals (biased exponent 0) are spaced 2^-133 apart, like the smallest normal
+    binade. With the exact ulp and U = 0 such a weight stays on its grid point; an update of
+    a fraction f of that spacing rounds up with probability f, which pins the spacing the
+    dither takes among the subnormals (half of it would round up never for f < 1/4, twice it
+    would round up 3/8 of the time at f = 1/4)."""
+    sub = np.arange(1, 128, dtype=np.uint16)                     # positive subnormal bf16 values
+    w0 = np.concatenate([sub, sub | np.uint16(0x8000)]).reshape(2, 127)
+    T = make(E, w0)
+    oracle.step([T], 1, exact_ulp=True)                          # zero gradients: U = 0
+    assert np.array_equal(T.w, w0)
+    n = 1 << 15
+    spacing = 2.0 ** -133
+    for frac in (0.25, 0.75):
+        base = np.full(n, 0x0040, np.uint16)                     # 64 * 2^-133
+        V = make(B, base + np.uint16(1))                          # backbone vector, exact V
+        V.g = bf16(np.full(n, 1e-2))                              # t = 1: U = sign(g) = 1
+        lr = float(np.float32((1.0 - frac) * spacing))           # exact in float32 (subnormal)
+        oracle.step([V], 1, lr=lr, clip_threshold=float("inf"), want_x=True, exact_ulp=True)
+        x = V.x_out.astype(np.float64)
+        assert np.allclose((x - 64 * spacing) / spacing, frac)
+        assert np.all((V.w == base) | (V.w == base + np.uint16(1)))
+        up = float(np.mean(V.w == base + np.uint16(1)))
+        assert abs(up - frac) < 4.0 * np.sqrt(frac * (1 - frac) / n) + 2e-3, (frac, up)

@@ -36,15 +36,22 @@
 extern "C" {
 #endif
 
-#define SKEW_ABI_VERSION 3
+#define SKEW_ABI_VERSION 4
 
 enum {
   SKEW_OK = 0,
   SKEW_EINVAL = -1,    /* bad argument: tier, ndim, shape, ld, NULL pointer, hyper-parameter */
   SKEW_ENOSPACE = -2,  /* a caller buffer is smaller than skew_state_bytes() asked for */
   SKEW_EHIP = -3,      /* the HIP runtime reported an error (launch, copy, memset) */
-  SKEW_ENOMEM = -4     /* host allocation of the context failed */
+  SKEW_ENOMEM = -4,    /* host allocation of the context failed */
+  SKEW_ESTALE = -5,    /* skew_step on a context whose static workspace a newer
+                          skew_state_init_static on the same GPU has taken over */
+  SKEW_ETOOBIG = -6    /* skew_state_init_static: the table needs more workspace than
+                          SKEW_STATIC_WORKSPACE_BYTES */
 };
+
+/* Bytes of the library's static workspace (skew_state_init_static), per GPU. */
+#define SKEW_STATIC_WORKSPACE_BYTES (64u << 20)
 
 enum { SKEW_TIER_BACKBONE = 0, SKEW_TIER_EXPERT = 1, SKEW_TIER_ROUTER = 2 };
 
@@ -169,13 +176,31 @@ int skew_state_bytes(const skew_tensor_desc *d, int n, size_t *state_bytes, size
 int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes,
                     void *workspace, size_t workspace_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): skew_state_init with the library's own
+ * static workspace in place of a caller buffer. The workspace is a file-scope device array
+ * of SKEW_STATIC_WORKSPACE_BYTES (64 MiB) that every GPU the library runs on holds until
+ * the process ends; this call and the steps of its context make no device allocation (the
+ * host context is an ordinary heap object, as with skew_state_init).
+ *   ctx, d, n, state, state_bytes, stream   as for skew_state_init.
+ * The array is shared by every call on one GPU and keeps the last call's contents: this
+ * call zero-fills the part its table uses. There is one such context per GPU at a time: a
+ * newer skew_state_init_static on the same GPU takes the array over, and skew_step on the
+ * older context then returns SKEW_ESTALE without launching anything. Steps of contexts
+ * that share the array must not overlap (they would race on it).
+ * Errors: as skew_state_init, and SKEW_ETOOBIG when skew_state_bytes() reports more than
+ * SKEW_STATIC_WORKSPACE_BYTES of workspace (nothing is touched then). */
+int skew_state_init_static(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes,
+                           void *stream);
+
 /* One SkewAdam step (Alg. 1) over every tensor of ctx, enqueued on `stream`
  * (asynchronous; errors of the kernels themselves surface at the caller's next
  * synchronisation). Reads g, updates w and the state in place. One step per
  * context may be in flight at a time. Non-finite gradients propagate into the
  * state and weights (a NaN makes the clip factor NaN, so its whole tensor).
  * The state's and workspace's contents between steps belong to the library.
- * Errors: SKEW_EINVAL (ctx NULL, hp invalid), SKEW_EHIP (launch failed). */
+ * Errors: SKEW_EINVAL (ctx NULL, hp invalid), SKEW_ESTALE (see skew_state_init_static),
+ * SKEW_EHIP (launch failed). */
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream);
 
 /* Free the host context. Does not touch device memory. NULL is a no-op. */

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -35,6 +36,7 @@ struct skew_ctx {
   float *gscale = nullptr;   // device: the gradient-norm mode's scale
   double *gsq = nullptr;     // device: per-tensor sums of g^2
   ItemList z[kZVariants];    // row-band pass items, one list per kernel variant
+  int static_dev = -1;       // >= 0: the workspace is the library's static one on this device
   // diagnostics: per recorded step, (launch kind, start event, end event) of every launch
   struct Timed {
     int kind;
@@ -48,6 +50,21 @@ struct skew_ctx {
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
   }
 };
+
+namespace {
+
+// The context that currently owns each device's static workspace (skew_state_init_static):
+// a newer one replaces it, and the older one's steps are then refused.
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+skew_ctx *g_static_owner[kMaxDevices] = {};
+
+bool static_owner_is(const skew_ctx *c) {
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  return c->static_dev >= 0 && c->static_dev < kMaxDevices && g_static_owner[c->static_dev] == c;
+}
+
+}  // namespace
 
 namespace {
 
@@ -104,6 +121,9 @@ const char *skew_strerror(int status) {
     case SKEW_ENOSPACE: return "a caller buffer is smaller than skew_state_bytes() requires";
     case SKEW_EHIP: return "HIP runtime error (launch, copy or memset failed)";
     case SKEW_ENOMEM: return "host allocation failed";
+    case SKEW_ESTALE:
+      return "this context's static workspace was taken over by a newer skew_state_init_static on its GPU";
+    case SKEW_ETOOBIG: return "the table needs more workspace than the library's static workspace holds";
     default: return "unknown status";
   }
 }
@@ -264,8 +284,36 @@ int skew_state_init(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, siz
                   static_cast<hipStream_t>(stream));
 }
 
+int skew_state_init_static(skew_ctx **ctx, skew_tensor_desc *d, int n, void *state, size_t state_bytes,
+                           void *stream) {
+  if (ctx == nullptr) return SKEW_EINVAL;
+  *ctx = nullptr;
+  Plan p;
+  int rc = plan_build(d, n, &p);
+  if (rc != SKEW_OK) return rc;
+  if (p.ws_bytes > static_workspace_bytes()) return SKEW_ETOOBIG;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SKEW_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return SKEW_EINVAL;
+  void *ws = nullptr;
+  if (static_workspace(&ws) != (int)hipSuccess || ws == nullptr) return SKEW_EHIP;
+  // the set-up below rewrites the array: from here on an older context on it is stale
+  {
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    g_static_owner[dev] = nullptr;
+  }
+  rc = init_ctx(ctx, p, d, n, state, state_bytes, static_cast<char *>(ws), static_workspace_bytes(),
+                static_cast<hipStream_t>(stream));
+  if (rc != SKEW_OK) return rc;
+  (*ctx)->static_dev = dev;
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  g_static_owner[dev] = *ctx;
+  return SKEW_OK;
+}
+
 int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   if (ctx == nullptr || !hparams_ok(hp)) return SKEW_EINVAL;
+  if (ctx->static_dev >= 0 && !static_owner_is(ctx)) return SKEW_ESTALE;
   StepConsts k = make_consts(*hp);
   k.gscale = ctx->gscale;
   k.gsq = ctx->gsq;
@@ -401,6 +449,12 @@ int skew_clip_info(skew_ctx *ctx, float *k, int32_t *route, int n, void *stream)
   return SKEW_OK;
 }
 
-void skew_destroy(skew_ctx *ctx) { delete ctx; }
+void skew_destroy(skew_ctx *ctx) {
+  if (ctx != nullptr && ctx->static_dev >= 0) {
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (g_static_owner[ctx->static_dev] == ctx) g_static_owner[ctx->static_dev] = nullptr;
+  }
+  delete ctx;
+}
 
 }  // extern "C"

@@ -195,6 +195,12 @@ inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a
 // Validates the table and computes sizes, offsets and the work-item lists.
 int plan_build(const skew_tensor_desc *d, int n, Plan *out);
 
+// The library's static workspace (skew_state_init_static): the device address of the
+// file-scope array on the current device, looked up once per device (skew_kernels.hip).
+// Returns a hipError_t value.
+int static_workspace(void **ptr);
+constexpr size_t static_workspace_bytes() { return (size_t)SKEW_STATIC_WORKSPACE_BYTES; }
+
 // Kernel launchers (skew_kernels.hip). Return a hipError_t value.
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream);
 // row-band pass, kernel variant log2(nseg) * 4 + (element loads ? 2 : 0) + (momentum ? 1 : 0)

@@ -21,6 +21,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "skew_internal.h"
@@ -2008,6 +2009,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 }
 
 }  // namespace
+
+// The static workspace of skew_state_init_static: device memory the library itself holds
+// on every GPU it runs on, for callers that cannot allocate. Host code never passes the
+// array's name to a kernel or a copy: it takes the array's device address on each device
+// from hipGetSymbolAddress (looked up once per device, with that device current).
+static __device__ __align__(256) unsigned char scratch[SKEW_STATIC_WORKSPACE_BYTES];
+
+int static_workspace(void **ptr) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDev] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return (int)e;
+  if (dev < 0 || dev >= kMaxDev) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (addr[dev] == nullptr) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return (int)hipSuccess;
+}
 
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream) {
   if (count <= 0) return hipSuccess;

@@ -14,16 +14,17 @@ from typing import Iterable, List, Optional, Sequence
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libskewadam.so")
 
-SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM = 0, -1, -2, -3, -4
+SKEW_OK, SKEW_EINVAL, SKEW_ENOSPACE, SKEW_EHIP, SKEW_ENOMEM, SKEW_ESTALE, SKEW_ETOOBIG = 0, -1, -2, -3, -4, -5, -6
+STATIC_WORKSPACE_BYTES = 64 << 20   # SKEW_STATIC_WORKSPACE_BYTES
 BACKBONE, EXPERT, ROUTER = 0, 1, 2
 FLAG_EXACT_CLIP = 1
 STATE_MOMENTUM, STATE_FACTORED, STATE_FP32 = 1, 2, 4   # tier variants (SKEW_STATE_*)
 FLAG_EXACT_ULP = 2
 TIERS = {"backbone": BACKBONE, "expert": EXPERT, "router": ROUTER}
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 # names every build of the library exports (checked by the CPU test suite)
-EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_step", "skew_destroy", "skew_strerror",
+EXPORTS = ("skew_state_bytes", "skew_state_init", "skew_state_init_static", "skew_step", "skew_destroy", "skew_strerror",
            "skew_abi_version", "skew_timing_enable", "skew_timing_read", "skew_launch_name", "skew_clip_info")
 
 
@@ -71,6 +72,9 @@ def lib():
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_size_t,
                                       ctypes.c_void_p]
         L.skew_state_init.restype = ctypes.c_int
+        L.skew_state_init_static.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_int,
+                                             ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.skew_state_init_static.restype = ctypes.c_int
         L.skew_step.argtypes = [ctypes.c_void_p, ctypes.POINTER(HParams), ctypes.c_void_p]
         L.skew_step.restype = ctypes.c_int
         L.skew_destroy.argtypes = [ctypes.c_void_p]
@@ -165,9 +169,12 @@ class SkewAdam:
     matrices; ``state_flags`` takes STATE_MOMENTUM / STATE_FACTORED (tier variants).
     The state and workspace are allocated here as torch byte tensors on the same
     device; weights, gradients and these buffers must outlive the object.
+    ``static_workspace=True`` sets the context up with skew_state_init_static: the
+    library's own static workspace replaces the workspace buffer (one such context per
+    GPU at a time; see include/skewadam.h).
     """
 
-    def __init__(self, params: Iterable, stream=None):
+    def __init__(self, params: Iterable, stream=None, static_workspace: bool = False):
         import torch
         params = list(params)
         self._keep = params
@@ -176,15 +183,21 @@ class SkewAdam:
         self.device = params[0][1].device if params else torch.device("cuda", torch.cuda.current_device())
         sb, wb = state_bytes(self.descs)
         self.state = torch.empty(max(sb, 1), dtype=torch.uint8, device=self.device)
-        self.workspace = torch.empty(max(wb, 1), dtype=torch.uint8, device=self.device)
+        self.workspace = None if static_workspace else torch.empty(max(wb, 1), dtype=torch.uint8, device=self.device)
         self.state_nbytes, self.workspace_nbytes = sb, wb
         self._arr = (TensorDesc * max(1, len(self.descs)))(*self.descs)
         ctx = ctypes.c_void_p()
         s = self._stream(stream)
-        rc = lib().skew_state_init(ctypes.byref(ctx), self._arr, len(self.descs), self.state.data_ptr(),
-                                   self.state.numel(), self.workspace.data_ptr(), self.workspace.numel(), s)
+        if static_workspace:
+            rc = lib().skew_state_init_static(ctypes.byref(ctx), self._arr, len(self.descs), self.state.data_ptr(),
+                                              self.state.numel(), s)
+            what = "skew_state_init_static"
+        else:
+            rc = lib().skew_state_init(ctypes.byref(ctx), self._arr, len(self.descs), self.state.data_ptr(),
+                                       self.state.numel(), self.workspace.data_ptr(), self.workspace.numel(), s)
+            what = "skew_state_init"
         if rc != SKEW_OK:
-            raise SkewError(rc, "skew_state_init")
+            raise SkewError(rc, what)
         self._ctx = ctx
         self._lib = lib()
 

@@ -135,6 +135,11 @@ int launch_clip(const DevTensor *T, const Item *items, int64_t count, const Step
 }
 int launch_recheck(const DevTensor *, RecheckLists *, int, const StepConsts &, int, void *) { return 0; }
 int launch_clip_recheck(const DevTensor *, RecheckLists *, int, const StepConsts &, int, void *) { return 0; }
+int static_workspace(void **ptr) {
+  static std::vector<char> buf(static_workspace_bytes());
+  *ptr = buf.data();
+  return 0;
+}
 }  // namespace skew
 
 // ---- the checks ----
@@ -414,6 +419,39 @@ int main() {
     check_init_and_step(gn ? "unit+gnorm" : "unit", unit, gn);
     check_init_and_step(gn ? "stacked+gnorm" : "stacked", stacked, gn);
     check_init_and_step(gn ? "variants+gnorm" : "variants", variants, gn);
+  }
+  // the static workspace: a second set-up on the same device makes the first one stale
+  {
+    std::vector<skew_tensor_desc> d = unit;
+    std::vector<std::vector<char>> data;
+    for (auto &x : d) {
+      data.emplace_back((size_t)(x.ndim == 1 ? x.rows * x.cols : x.rows * x.ld) * 2 + 16);
+      x.w = data.back().data();
+      x.g = data.back().data();
+    }
+    size_t sb = 0, wb = 0;
+    skew_state_bytes(d.data(), (int)d.size(), &sb, &wb);
+    std::vector<char> s1(sb), s2(sb);
+    skew_ctx *a = nullptr, *b = nullptr;
+    g_buf = Buffers{nullptr, nullptr, 0, 0, 0};
+    g_buf.ws = nullptr;
+    CHECK(skew_state_init_static(&a, d.data(), (int)d.size(), s1.data(), sb, nullptr) == SKEW_OK, "static init 1");
+    CHECK(skew_state_init_static(&b, d.data(), (int)d.size(), s2.data(), sb, nullptr) == SKEW_OK, "static init 2");
+    skew_hparams hp{3e-4f, 0.9f, 0.999f, 1e-8f, 1.0f, 0, 1, 0, 0.0f, 0.0f};
+    void *sw = nullptr;
+    static_workspace(&sw);
+    g_buf = Buffers{s2.data(), static_cast<char *>(sw), sb, static_workspace_bytes(), 0};
+    Plan p;
+    plan_build(d.data(), (int)d.size(), &p);
+    g_buf.nt = (int)p.t.size();
+    CHECK(skew_step(a, &hp, nullptr) == SKEW_ESTALE, "the older static context is stale");
+    CHECK(skew_step(b, &hp, nullptr) == SKEW_OK, "the newer static context steps");
+    skew_destroy(a);
+    skew_destroy(b);
+    skew_ctx *c = nullptr;
+    CHECK(skew_state_init_static(&c, big.data(), (int)big.size(), nullptr, 0, nullptr) == SKEW_ETOOBIG,
+          "a table beyond the static workspace");
+    CHECK(c == nullptr, "no context on failure");
   }
   // validation: bad descriptors are refused before anything is touched
   {

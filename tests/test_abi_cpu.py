@@ -26,8 +26,8 @@ def test_library_exports_every_declared_function():
     L = ctypes.CDLL(P.skewadam.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
-    assert P.lib().skew_abi_version() == P.skewadam.ABI_VERSION == 3
-    for code in (0, -1, -2, -3, -4, -99):
+    assert P.lib().skew_abi_version() == P.skewadam.ABI_VERSION == 4
+    for code in (0, -1, -2, -3, -4, -5, -6, -99):
         assert P.lib().skew_strerror(code)
 
 
@@ -167,3 +167,18 @@ def test_binding_refuses_missing_library(tmp_path, monkeypatch):
     monkeypatch.setattr(P.skewadam, "_LIB", None)
     with pytest.raises(RuntimeError):
         P.skewadam.lib()
+
+
+def test_static_workspace_refuses_tables_beyond_its_size():
+    """skew_state_init_static sizes the table before it touches any device: a table whose
+    workspace exceeds the 64 MiB static array is refused (SKEW_ETOOBIG) on the host."""
+    import ctypes
+    wl = W.get("layer")
+    descs = _descs(wl)
+    _, wb = P.state_bytes(descs)
+    assert wb > P.skewadam.STATIC_WORKSPACE_BYTES
+    arr = (P.TensorDesc * len(descs))(*descs)
+    ctx = ctypes.c_void_p()
+    rc = P.lib().skew_state_init_static(ctypes.byref(ctx), arr, len(descs), None, 0, None)
+    assert rc == P.skewadam.SKEW_ETOOBIG and not ctx.value
+    assert b"static workspace" in P.lib().skew_strerror(rc)

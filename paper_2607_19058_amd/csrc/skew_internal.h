@@ -80,6 +80,8 @@ struct BandStats {
   float rmax;     // max R_i
   int32_t bad;    // a row with R_i == 0 but a nonzero gradient (its elements escape the bounds)
   int32_t regime; // the sums this band formed (kRegime*)
+  int32_t rdup;   // rows whose R_i > 0 equals the previous row's (repeated factors)
+  int32_t pad;
 };
 
 // Per fold chunk of columns of a row-band tensor.
@@ -88,7 +90,7 @@ struct ColStats {
   float cmin;     // min c'_j over columns with C_j > 0 (+inf if none)
   float cmax;     // max c'_j
   int32_t bad;    // non-finite c'_j, or C_j == 0 with a nonzero column sum
-  int32_t pad;
+  int32_t cdup;   // columns whose C_j > 0 equals the previous column's within the chunk
 };
 
 // Device-resident description of one tensor, its state and its partial sums.

@@ -953,10 +953,11 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // the band's R and 1/sqrt(R) (coalesced), and its statistics: fixed-order reductions
   // (mode 1: the band's sum of g^2 instead; mode 2: R was written by the fold)
   const int64_t nrows = r1 - r0;
-  double rs = rs_l;
+  double rs = rs_l, rdup = 0.0;
   float rmn = __builtin_inff(), rmx = 0.f;
   for (int64_t j = threadIdx.x; mode != 1 && j < nrows; j += kZThreads) {
     const float R = rstash[j];
+    if (j > 0 && R > 0.f && R == rstash[j - 1]) rdup += 1.0;
     const double Rd = (double)R;
     const bool normal = R > 0.f && R < __builtin_inff();
     if (mode == 0) {
@@ -973,7 +974,9 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   const float rmin = wg_min_wf<kZWaves>(rmn, sh);
   const float rmax = wg_max_wf<kZWaves>(rmx, sh);
   const int bd = wg_or_w<kZWaves>(bad_l, sh);
+  const double rd = wg_sum_w<kZWaves>(rdup, sh);
   if (threadIdx.x == 0) {
+    stg(&t.bst[band].rdup, (int32_t)rd);
     stg(&t.bst[band].rsum, rsum);
     stg(&t.bst[band].ysum, ys);
     stg(&t.bst[band].umax, um);
@@ -1109,10 +1112,11 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
   } else {
     // row-band tensor: C_j (phase 0; phase 2 has it from phase 1), c'_j = C_j / max(mean R,
     // eps) and sum_j z_j / c'_j over the chunk
+    __shared__ float cprev[kThreads];
     const float q = mean_r_clamped(t, k, sh);
     const int64_t j = (int64_t)it.tile * kFold + threadIdx.x;
     double sj = 0.0;
-    float cmn = __builtin_inff(), cmx = 0.f;
+    float cmn = __builtin_inff(), cmx = 0.f, Cj = 0.f;
     int bad = 0;
     if (j < t.m) {
       double cs = 0.0, zs = 0.0;
@@ -1130,6 +1134,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
       } else {
         C = ldg(t.C + j);
       }
+      Cj = C;
       const float cp = C / q;
       if (C > 0.f) {
         // c'_j that is zero or not finite leaves the tensor to the exact pass
@@ -1143,11 +1148,17 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
         bad = 1;   // NaN, or a nonzero column whose C underflowed
       }
     }
+    // repeated column factors: C_j equal to the previous column's (within the chunk)
+    cprev[threadIdx.x] = Cj;
+    __syncthreads();
+    const double dup = (threadIdx.x > 0 && Cj > 0.f && Cj == cprev[threadIdx.x - 1]) ? 1.0 : 0.0;
     const double S = block_sum(sj, sh);
+    const double cdup = block_sum(dup, sh);
     const float cmin = wg_min_wf<kWaves>(cmn, sh);
     const float cmax = wg_max_wf<kWaves>(cmx, sh);
     const int b = wg_or_w<kWaves>(bad, sh);
     if (threadIdx.x == 0) {
+      stg(&t.cst[it.tile].cdup, (int32_t)cdup);
       stg(&t.cst[it.tile].s, S);
       stg(&t.cst[it.tile].cmin, cmin);
       stg(&t.cst[it.tile].cmax, cmax);
@@ -1610,18 +1621,64 @@ __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor 
 // its unfloored and its floored value, up to rounding).
 struct SliceSum {
   double S, E;
-  int open;   // 0, or why the sum is open (kWhyStraddle, kWhyMissingSum)
-  int bad;    // a non-finite sum or statistic
+  int open;     // 0, or why the sum is open (kWhyStraddle, kWhyMissingSum)
+  int bad;      // a non-finite sum or statistic
+  int repeats;  // the R_i or the c'_j repeat: the spread of the fast sum is not statistical
 };
+
+// The spread bounds of the fast sums take the roundings of R_i c'_j, of the square root and
+// of the quotient as independent from element to element. When the R_i or the C_j of a
+// factored tensor repeat (all equal, as under a constant gradient, or many equal neighbours,
+// as under a gradient of a few distinct magnitudes), the first two roundings repeat with
+// them and do not average out. Such a tensor takes the rigorous bound instead: each term of
+// the fast sum lies within 5.05 u (u = 2^-24) of the oracle's rounded U_hat^2.
+constexpr double kRigorousRel = 5.05 * 0x1p-24;
+// all (nearly) equal, or more than 1/64 of neighbours equal (never seen with gradients of
+// continuous distribution: R_i and C_j are sums of many squares); the extremes are over
+// positive values (of R and C, or of R and c' = C / q: the same ratio)
+__device__ __forceinline__ int repeats_rule(const DevTensor &t, float rmn, float rmx, float cmn, float cmx,
+                                            double dup_r, double dup_c) {
+  const bool ur = t.n > 1 && rmx <= rmn * (1.f + 0x1p-20f);
+  const bool uc = t.m > 1 && cmx <= cmn * (1.f + 0x1p-20f);
+  return (ur || uc || 64.0 * dup_r > (double)t.n || 64.0 * dup_c > (double)t.m) ? 1 : 0;
+}
+// wide factored tensors: a scan of R and C (the row-band tensors have these in their band
+// and column-chunk statistics)
+template <class Red>
+__device__ __forceinline__ int repeated_factors(const DevTensor &t, const Red &r) {
+  double dup_r = 0.0, dup_c = 0.0;
+  float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
+  for (int64_t i = r.lane(); i < t.n; i += Red::kN) {
+    const float a = ldg(t.R + i);
+    if (i > 0 && a > 0.f && a == ldg(t.R + i - 1)) dup_r += 1.0;
+    if (a > 0.f) rmn = fminf(rmn, a);
+    rmx = fmaxf(rmx, a);
+  }
+  for (int64_t j = r.lane(); j < t.m; j += Red::kN) {
+    const float a = ldg(t.C + j);
+    if (j > 0 && a > 0.f && a == ldg(t.C + j - 1)) dup_c += 1.0;
+    if (a > 0.f) cmn = fminf(cmn, a);
+    cmx = fmaxf(cmx, a);
+  }
+  dup_r = r.sum(dup_r);
+  dup_c = r.sum(dup_c);
+  rmn = r.minf(rmn);
+  rmx = r.maxf(rmx);
+  cmn = r.minf(cmn);
+  cmx = r.maxf(cmx);
+  return repeats_rule(t, rmn, rmx, cmn, cmx, dup_r, dup_c);
+}
+
 template <class Red>
 __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepConsts &k, const Red &r) {
-  SliceSum o = {0.0, 0.0, 0, 0};
+  SliceSum o = {0.0, 0.0, 0, 0, 0};
   const float q = t.kind == kFactored ? mean_r_of(t, k, r) : 0.f;
+  if (t.kind == kFactored && !t.zpath) o.repeats = repeated_factors(t, r);
   if (t.zpath) {
     const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
     const double Y = red_sum(r, &t.bst->ysum, t.nzb, bstride);
     const double SU = red_sum(r, &t.cst->s, t.nfc, cstride);
-    double um = 0.0;
+    double um = 0.0, dup_r = 0.0, dup_c = 0.0;
     float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
     int bad = 0;
     for (int64_t b = r.lane(); b < t.nzb; b += Red::kN) {
@@ -1629,11 +1686,13 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
       rmn = fminf(rmn, ldg(&t.bst[b].rmin));
       rmx = fmaxf(rmx, ldg(&t.bst[b].rmax));
       bad |= ldg(&t.bst[b].bad);
+      dup_r += (double)ldg(&t.bst[b].rdup);
     }
     for (int64_t c = r.lane(); c < t.nfc; c += Red::kN) {
       cmn = fminf(cmn, ldg(&t.cst[c].cmin));
       cmx = fmaxf(cmx, ldg(&t.cst[c].cmax));
       bad |= ldg(&t.cst[c].bad);
+      dup_c += (double)ldg(&t.cst[c].cdup);
     }
     um = r.max(um);
     rmn = r.minf(rmn);
@@ -1641,6 +1700,7 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
     cmn = r.minf(cmn);
     cmx = r.maxf(cmx);
     bad = r.any(bad);
+    o.repeats = repeats_rule(t, rmn, rmx, cmn, cmx, r.sum(dup_r), r.sum(dup_c));
     // the sums the row-band pass formed this step (it skips one when the last step
     // predicts the regime); a sum it did not form counts as +inf
     const int formed = ldg(&t.bst[0].regime);
@@ -1655,6 +1715,7 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
     } else if (have_z && lo >= k.eps) {   // nothing on the floor
       o.S = SU;
       o.E = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) + 1e-14 * SU : 0.0;
+      if (o.repeats) o.E = fmax(o.E, kRigorousRel * SU + 1e-14 * SU);
     } else if (have_y && hi < k.eps) {    // everything on the floor
       o.S = Y;
       o.E = 1e-14 * Y;
@@ -1674,6 +1735,7 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
     // the exact second moment's sum is the oracle's own; a factored one carries the
     // spread of its unrounded terms (20 standard deviations)
     o.E = t.kind == kFactored ? 20.0 * 0x1p-23 * sqrt(Q4) + 1e-14 * o.S : 0.0;
+    if (o.repeats) o.E = fmax(o.E, kRigorousRel * o.S + 1e-14 * o.S);
   }
   if (r.lead()) stg(&t.sc->q, q);
   return o;
@@ -1693,7 +1755,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
                                                         RecheckLists *L, int ntensors) {
   __shared__ double sh[kThreads];
   __shared__ double wsum[kWaves][3];
-  __shared__ int wflag[kWaves][3];
+  __shared__ int wflag[kWaves][4];
   __shared__ float kf_sh;
   __shared__ int st_sh, pos_sh;
   const Item it = items[blockIdx.x];   // the first sub-tensor of a group sharing one k
@@ -1703,7 +1765,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   // error bounds, in slice order within a wave and then wave by wave
   double S = 0.0, err = 0.0, N = 0.0;
   int open = 0;   // why the first open slice (in slice order) is open
-  bool bad_any = false;
+  bool bad_any = false, rep_any = false;
   if (ng == 1) {
     const SliceSum o = slice_sum(t0, k, RedGroup{sh});
     S = o.S;
@@ -1711,10 +1773,11 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     N = (double)(t0.n * t0.m);
     open = o.open;
     bad_any = o.bad != 0;
+    rep_any = o.repeats != 0;
   } else {
     const int w = (int)(threadIdx.x >> 6);
     double s = 0.0, e_ = 0.0, nn = 0.0;
-    int first = 0x7fffffff, why = 0, bad = 0;   // the wave's first open slice, and why it is open
+    int first = 0x7fffffff, why = 0, bad = 0, rep = 0;   // the wave's first open slice, and why it is open
     for (int e = w; e < ng; e += kWaves) {
       const DevTensor &t = TT[g0 + e];
       const SliceSum o = slice_sum(t, k, RedWave{});
@@ -1726,6 +1789,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
         why = o.open;
       }
       bad |= o.bad;
+      rep |= o.repeats;
     }
     if ((threadIdx.x & 63) == 0) {
       wsum[w][0] = s;
@@ -1734,6 +1798,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       wflag[w][0] = first;
       wflag[w][1] = why;
       wflag[w][2] = bad;
+      wflag[w][3] = rep;
     }
     __syncthreads();
     int f = 0x7fffffff;
@@ -1746,6 +1811,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
         open = wflag[v][1];
       }
       bad_any |= wflag[v][2] != 0;
+      rep_any |= wflag[v][3] != 0;
     }
   }
   if (threadIdx.x == 0) {
@@ -1760,7 +1826,9 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       S += err;   // an upper bound of the group's sum
       if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
         amb = true;
-        level = 1;   // the floor split per element decides most of these
+        // the floor split per element decides most of these, except where the factors
+        // repeat (its spread is statistical too)
+        level = rep_any ? 2 : 1;
       }
     } else {
       spread = S > 0.0 ? err / S : 0.0;

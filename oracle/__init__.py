@@ -92,6 +92,10 @@ def lib():
         L.skew_oracle_u16.restype = ctypes.c_uint32
         L.skew_oracle_u16_array.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p]
         L.skew_oracle_threads.restype = ctypes.c_int
+        L.skew_oracle_sumsq_bf16.argtypes = [ctypes.c_void_p, ctypes.c_int64]
+        L.skew_oracle_sumsq_bf16.restype = ctypes.c_double
+        L.skew_oracle_set_threads.argtypes = [ctypes.c_int]
+        L.skew_oracle_set_threads.restype = None
         _LIB = L
     return _LIB
 
@@ -251,6 +255,17 @@ def dither_u16(key: int, idx0: int, n: int) -> np.ndarray:
 
 def threads() -> int:
     return int(lib().skew_oracle_threads())
+
+
+def sumsq_bf16(g: np.ndarray) -> float:
+    """Sum of squares in double of bf16 values (uint16 bits): a set's squared gradient norm."""
+    g = np.ascontiguousarray(g, np.uint16)
+    return float(lib().skew_oracle_sumsq_bf16(g.ctypes.data, g.size))
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of later oracle steps (the results do not depend on the count)."""
+    lib().skew_oracle_set_threads(int(n))
 
 
 # ----------------------------------------------------------------------------------------

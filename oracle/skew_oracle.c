@@ -143,6 +143,34 @@ int skew_oracle_threads(void) {
 #endif
 }
 
+double skew_oracle_sumsq_bf16(const uint16_t *g, int64_t n) {
+  /* fixed chunks summed in order, each chunk in ascending index order */
+  const int64_t chunk = 1 << 20, nc = (n + chunk - 1) / chunk;
+  double *part = (double *)calloc((size_t)(nc > 0 ? nc : 1), sizeof(double));
+#pragma omp parallel for schedule(static)
+  for (int64_t c = 0; c < nc; c++) {
+    const int64_t e = (c + 1) * chunk < n ? (c + 1) * chunk : n;
+    double s = 0.0;
+    for (int64_t i = c * chunk; i < e; i++) {
+      const double v = bf16_bits_to_f32(g[i]);
+      s += v * v;
+    }
+    part[c] = s;
+  }
+  double total = 0.0;
+  for (int64_t c = 0; c < nc; c++) total += part[c];
+  free(part);
+  return total;
+}
+
+void skew_oracle_set_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 static float max_nan(float a, float b) { return (a != a) ? a : (a < b ? b : a); }
 
 /* Eq. 1 and the rank-one reconstruction for one n x m matrix (one slice of a stacked

@@ -80,6 +80,11 @@ uint64_t skew_oracle_key(uint64_t seed, int64_t step, uint64_t tensor_id);
 uint32_t skew_oracle_u16(uint64_t key, uint64_t idx);
 void skew_oracle_u16_array(uint64_t key, uint64_t idx0, int64_t n, uint32_t *out);
 int skew_oracle_threads(void);
+/* Sum of squares of n bf16 values in double (squares of bf16 values are exact in double):
+ * the squared gradient norm of a whole set, for steps over a sample of it (gsq_total). */
+double skew_oracle_sumsq_bf16(const uint16_t *g, int64_t n);
+/* Sets the OpenMP thread count of later steps (results do not depend on it). */
+void skew_oracle_set_threads(int n);
 
 #ifdef __cplusplus
 }

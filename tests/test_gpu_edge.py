@@ -11,7 +11,7 @@ import oracle
 from paper_2607_19058_amd import SkewAdam
 from paper_2607_19058_amd import workloads as W
 
-from parity_util import log, run
+from parity_util import ParityRun, log, run
 
 pytestmark = pytest.mark.gpu
 
@@ -121,10 +121,15 @@ def test_row_band_widths_with_partial_chunks(hp):
     the block loads mask the lanes past the row (for M, each of its two 1 KiB halves on its
     own) and the last block of a band holds rows past the band's end. Widths of 2, 4, 9 and
     17 chunks take one to four chunks per wave (17: the general load loop); every tensor
-    compared."""
+    compared. Also the widest row-band rows: 11008 columns (22 chunks, the ragged mix's
+    experts) and 16384 columns (32 chunks, the row-band limit), with and without momentum,
+    and 16392 columns, the first width past it (pass 1 by tiles instead)."""
     shapes = [("bb.w1000", W.BACKBONE, (300, 1000)), ("bb.w1544", W.BACKBONE, (70, 1544)),
               ("bb.w4104", W.BACKBONE, (33, 4104)), ("bb.w8200", W.BACKBONE, (40, 8200)),
               ("ex.w1544", W.EXPERT, (96, 1544)), ("ex.w8200", W.EXPERT, (24, 8200)),
+              ("ex.w11008", W.EXPERT, (37, 11008)), ("bb.w11008", W.BACKBONE, (19, 11008)),
+              ("ex.w16384", W.EXPERT, (21, 16384)), ("bb.w16384", W.BACKBONE, (9, 16384)),
+              ("ex.w16392", W.EXPERT, (11, 16392)),
               ("rt", W.ROUTER, (256, 8))]
     specs = [W.Spec(name, tier, shape, k) for k, (name, tier, shape) in enumerate(shapes)]
     wl = W.Workload("partial_chunks", specs, 4)
@@ -164,3 +169,46 @@ def test_overlapping_row_views_are_refused_before_any_launch():
     torch.cuda.synchronize()
     assert torch.count_nonzero(base) == 0
 
+
+
+def test_structured_gradients_clip_factor_matches_the_oracle():
+    """Gradients whose R_i or C_j repeat (a constant gradient; a rank-one gradient of two
+    magnitudes per row and per column): the roundings of R_i c'_j and of the square root then
+    repeat and do not average out, so the clip stage must not trust a statistical spread. With
+    clipping active (threshold 0.5), every clip factor (skew_clip_info) equals the oracle's
+    float bit for bit, and weights and state meet the parity bar. Row-band tensors with and
+    without momentum, a wide tensor (pass 1 by tiles) and a stacked tensor."""
+    import numpy as np
+    shapes = [("ex.const", W.EXPERT, (256, 1024)), ("ex.rank1", W.EXPERT, (512, 512)),
+              ("bb.const", W.BACKBONE, (128, 2048)), ("bb.rank1", W.BACKBONE, (96, 1536)),
+              ("ex.wide_const", W.EXPERT, (16, 16392)), ("ex.stack_const", W.EXPERT, (4, 64, 512)),
+              ("rt", W.ROUTER, (64, 8))]
+    specs = [W.Spec(name, tier, shape, k) for k, (name, tier, shape) in enumerate(shapes)]
+    wl = W.Workload("structured", specs, 5)
+    hp = dict(oracle.DEFAULTS, clip_threshold=0.5)
+
+    def structured(t, G):
+        for k, s in enumerate(specs):
+            if s.tier == W.ROUTER:
+                continue
+            if "rank1" in s.name:
+                n, m = s.shape
+                a = torch.where(torch.arange(n, device=G[k].device) % 3 == 0, 1.5, 1.0)
+                b = torch.where(torch.arange(m, device=G[k].device) % 5 == 0, 1.5, 1.0)
+                sign = torch.where((torch.arange(n * m, device=G[k].device).view(n, m) * 7 + t) % 11 < 5, -1.0, 1.0)
+                G[k].copy_(sign * (2e-3 * (1 + 0.25 * t)) * a[:, None] * b[None, :])
+            else:
+                G[k].fill_(2e-3 * (1 + 0.25 * t))
+
+    pr = ParityRun(wl, hp=hp)
+    routes_seen = set()
+    for t in range(1, 6):
+        pr.step(t, mutate=structured)
+        kk, route = pr.opt.clip_info()
+        for k, s in enumerate(specs):
+            o = pr.O[k]
+            k_oracle = np.float32(1.0 / max(1.0, o.rms / hp["clip_threshold"]))
+            assert np.float32(kk[k]).view(np.uint32) == k_oracle.view(np.uint32), (s.name, t, kk[k], k_oracle)
+            routes_seen.add(route[k] & 0xF)
+    log(f"  total: {pr.stats}; clip routes seen {sorted(routes_seen)}")
+    assert pr.stats.ok(), pr.stats

@@ -2,8 +2,10 @@
 
 Workloads: the tiny one-layer MoE on every tensor, unit shapes (odd, ragged, strided,
 unaligned, vectors), and the full-size workloads (one MoE layer at width 2048, the
-heavy-tailed stress case, the ragged tier mix, and the 6.78B parameter set) on
-sampled tensors. Every test calls the library through its C ABI.
+heavy-tailed stress case, the ragged tier mix, and the 6.78B parameter set) with every
+tensor compared at chosen steps (each compared step starts the oracle from the GPU's
+weights and state before it), plus sampled tensors followed over all steps of the 6.78B
+and ragged runs. Every test calls the library through its C ABI.
 """
 import os
 
@@ -15,7 +17,7 @@ import oracle
 from paper_2607_19058_amd import SkewAdam
 from paper_2607_19058_amd import workloads as W
 
-from parity_util import ParityRun, bits, log, run
+from parity_util import ParityRun, StreamParity, bits, log, run
 
 pytestmark = pytest.mark.gpu
 
@@ -60,14 +62,17 @@ def test_unit_shapes_all_tiers():
 
 
 def test_strided_and_unaligned_tensors():
-    """Row stride larger than the width, and pointers off 16-byte alignment: the
-    scalar path must give the same bits as the oracle on the dense copy."""
+    """Row stride larger than the width, and pointers off 16-byte alignment (the scalar
+    paths): weights and every state array against the oracle on the dense copy, to the same
+    bar as every other parity test; the padding around each view stays untouched."""
     log("[parity] strided / unaligned tensors")
     dev = torch.device("cuda")
     wl = W.Workload("strided", [W.Spec("a", W.EXPERT, (37, 200), 0), W.Spec("b", W.BACKBONE, (64, 1024), 1),
-                                W.Spec("c", W.ROUTER, (16, 24), 2)], 3)
+                                W.Spec("c", W.ROUTER, (16, 24), 2), W.Spec("d", W.EXPERT, (40, 1031), 3),
+                                W.Spec("e", W.BACKBONE, (33, 520), 4)], 3)
+    pads, offs = (56, 8, 3, 5, 16), (0, 1, 1, 3, 8)
     bases, Ws, Gs = [], [], []
-    for s, pad, off in zip(wl.specs, (56, 8, 3), (0, 1, 1)):
+    for s, pad, off in zip(wl.specs, pads, offs):
         n, m = s.shape
         wb = torch.zeros((n, m + pad + off), dtype=torch.bfloat16, device=dev)
         gb = torch.zeros_like(wb)
@@ -76,53 +81,88 @@ def test_strided_and_unaligned_tensors():
         bases.append((wb, gb))
         Ws.append(w)
         Gs.append(gb[:, off:off + m])
-    opt = SkewAdam([(s.tier, Ws[k], Gs[k], s.tensor_id) for k, s in enumerate(wl.specs)])
-    O = [oracle.Tensor(tier=s.tier, w=bits(Ws[k]).copy(), g=np.zeros(s.shape, np.uint16),
-                       tensor_id=s.tensor_id).init_state() for k, s in enumerate(wl.specs)]
+    pr = ParityRun(wl, weights=Ws, grads=Gs, hp=dict(oracle.DEFAULTS, lr=1e-2))
     for t in range(1, 4):
-        for k, s in enumerate(wl.specs):
-            g = torch.empty(s.shape, dtype=torch.bfloat16, device=dev)
-            W.fill_grad(s, wl, t, g)
-            Gs[k].copy_(g)
-            O[k].g = bits(g)
-        opt.step(t, lr=1e-2)
-        oracle.step(O, t, lr=1e-2, want_y=True)
-        torch.cuda.synchronize()
-        for k, s in enumerate(wl.specs):
-            gw = bits(Ws[k])
-            diff = gw != O[k].w
-            if diff.any():
-                from parity_util import near_boundary
-                assert near_boundary(O[k].y_out[diff]).all(), (s.name, t, int(diff.sum()))
-            assert diff.mean() <= 1e-3, (s.name, t)
-            # padding columns are untouched
-            wb, gb = bases[k]
-            n, m = s.shape
-            assert torch.count_nonzero(wb[:, :(0, 1, 1)[k]]) == 0
-            assert torch.count_nonzero(wb[:, (0, 1, 1)[k] + m:]) == 0
+        pr.step(t)
+    assert pr.stats.ok(), pr.stats
+    assert pr.stats.compared == 3 * sum(s.numel for s in wl.specs)
+    for k, s in enumerate(wl.specs):
+        wb, gb = bases[k]
+        n, m = s.shape
+        assert torch.count_nonzero(wb[:, :offs[k]]) == 0
+        assert torch.count_nonzero(wb[:, offs[k] + m:]) == 0
 
 
-def test_layer_sampled():
+def _route_log(routes, specs):
+    counts = {r: sum(1 for q, s in zip(routes, specs) if q == r and s.numel > 0) for r in (0, 4, 2)}
+    return ", ".join(f"{StreamParity.ROUTES[r]}: {c}" for r, c in counts.items())
+
+
+def _every_tensor(wl, compare_steps, max_steps, need_routes=False):
+    """Run `wl` on the GPU and compare every tensor at the steps in compare_steps, and (with
+    need_routes) at further steps until each way of deciding the clip factor (fast sums,
+    floor-split re-check, exact re-check; no forcing flag) has been taken by a compared
+    tensor. Returns the routes seen on compared steps."""
+    sp = StreamParity(wl)
+    seen = set()
+    done = 0
+    for t in range(1, max_steps + 1):
+        routes = sp.step(t, snapshot=True)
+        here = {r for r, s in zip(routes, wl.specs) if s.numel > 0}
+        want = t in compare_steps or (need_routes and not here <= seen)
+        if want:
+            st = sp.compare_last()
+            assert st.ok(), (t, st)
+            log(f"    routes at step {t}: {_route_log(routes, wl.specs)}")
+            seen |= here
+            done += 1
+        if done >= len(compare_steps) and (not need_routes or seen >= {0, 2, 4}):
+            break
+    log(f"  total: {sp.stats}")
+    assert sp.stats.ok(), sp.stats
+    return seen
+
+
+@pytest.mark.timeout(900)
+def test_layer_every_tensor():
+    """One MoE layer at full width (263 tensors, 4.35B parameters), 5 steps, every tensor
+    compared at the last."""
     wl = W.get("layer")
-    names = {s.name: s.tensor_id for s in wl.specs}
-    sc = W.expert_scales(wl, 1)[0]
-    zero_e = int(np.flatnonzero(sc == 0)[0])
-    small_e = int(np.argsort(np.where(sc > 0, sc, np.inf))[0])
-    big_e = int(np.argmax(sc))
-    sample = [names["attn.0"], names["ffn.down"], names[f"ex{zero_e}.up"], names[f"ex{small_e}.down"],
-              names[f"ex{big_e}.up"], names["ex7.down"], names["router"]]
-    log(f"[parity] layer: 263 tensors (4.35B params), 5 steps, sampled {sample}")
-    st = run(wl, sample=sample)
-    assert st.ok(), st
+    log("[parity] layer: 263 tensors (4.35B params), 5 steps, every tensor compared at step 5")
+    _every_tensor(wl, {5}, 5)
 
 
-def test_stress_sampled():
+@pytest.mark.timeout(900)
+def test_stress_every_tensor_and_clip_routes():
+    """Heavy-tailed stress (Student-t(2), 0.1% outliers x100, 90% sparse experts): every
+    tensor at each of its 5 steps, and each way of deciding the clip factor taken by at least
+    one compared tensor (fast sums, floor-split re-check, exact re-check), unforced."""
     wl = W.get("stress")
-    names = {s.name: s.tensor_id for s in wl.specs}
-    sample = [names["attn.1"], names["ffn.up"], names["ex3.up"], names["ex64.down"], names["router"]]
-    log(f"[parity] stress: Student-t(2) gradients with outliers and 90% sparse experts, sampled {sample}")
-    st = run(wl, sample=sample)
-    assert st.ok(), st
+    log("[parity] stress: 263 tensors, 5 steps, every tensor compared")
+    seen = _every_tensor(wl, {1, 2, 3, 4, 5}, 5)
+    assert seen >= {0, 2, 4}, f"clip routes taken on compared steps: {sorted(seen)}"
+
+
+@pytest.mark.timeout(900)
+def test_full_every_tensor_and_clip_routes():
+    """The benchmark workload (6.78B parameters, 432 tensors; tok_embed and the untied head
+    included) in bench.py's launch configuration: every tensor compared at steps 1-3 and at
+    later steps until each way of deciding the clip factor has been taken by a compared
+    tensor (unforced)."""
+    wl = W.get("full")
+    log("[parity] full 6.78B: 432 tensors, every tensor compared at steps 1-3 and until every clip route is seen")
+    seen = _every_tensor(wl, {1, 2, 3}, 20, need_routes=True)
+    assert seen >= {0, 2, 4}, f"clip routes taken on compared steps: {sorted(seen)}"
+
+
+@pytest.mark.timeout(900)
+def test_ragged_every_tensor():
+    """The ragged tier mix (269 tensors, 7.05B parameters: 1536/6144/4096/11008-column
+    matrices, 1-D vectors on the exact fallback): every tensor compared at step 2 (a sample is
+    followed over all 50 steps below)."""
+    wl = W.get("ragged")
+    log("[parity] ragged: 269 tensors (7.05B params), every tensor compared at step 2")
+    _every_tensor(wl, {2}, 2)
 
 
 def test_determinism_order_and_resume():
@@ -183,14 +223,15 @@ def test_hparam_errors_launch_nothing():
 def test_full_6p78b_sampled():
     """The benchmark workload (6,784,327,680 parameters, 432 tensors), all 20 steps, in the
     launch configuration bench.py times; the oracle follows a sample of tensors from every
-    tier (norm vector, attention, positions, expert matrices of both orientations including a
-    zero-gradient one, a router)."""
+    tier (norm vector, attention, positions, the 50304x2048 embedding and the untied
+    2048x50304 head, expert matrices of both orientations including a zero-gradient one, a
+    router)."""
     wl = W.get("full")
     names = {s.name: s.tensor_id for s in wl.specs}
     sc = W.expert_scales(wl, 1)[0]
     zero_e = int(np.flatnonzero(sc == 0)[0])
-    sample = [names["norm.3"], names["attn.7"], names["pos_embed"], names["ex5.gate"], names["ex77.down"],
-              names[f"ex{zero_e}.up"], names["router.1"]]
+    sample = [names["norm.3"], names["attn.7"], names["pos_embed"], names["tok_embed"], names["lm_head"],
+              names["ex5.gate"], names["ex77.down"], names[f"ex{zero_e}.up"], names["router.1"]]
     log(f"[parity] full 6.78B: 432 tensors, 20 steps, sampled {sample}")
     st = run(wl, sample=sample)
     assert st.ok(), st
@@ -202,7 +243,7 @@ def test_ragged_sampled():
     wl = W.get("ragged")
     names = {s.name: s.tensor_id for s in wl.specs}
     sample = [names["norm.1"], names["bias.2"], names["attn.0"], names["exA3.up"], names["exA9.down"],
-              names["exB40.down"], names["router"]]
+              names["exB40.down"], names["exB7.up"], names["router"]]
     log(f"[parity] ragged: 269 tensors (7.05B params), 50 steps, sampled {sample}")
     st = run(wl, sample=sample)
     assert st.ok(), st

@@ -7,20 +7,26 @@ sizes of the paper's model), bf16 weights and gradients resident in HBM.
 
 One timed step is one call of skew_step over every tensor, i.e. the whole hot path
 (row-band statistics, fold, update sums, clip factor, update and dithered write-back).
-W warmup steps draw fresh seeded gradients; the K timed steps then run back to back
-on the resident gradient of one further draw, with the step counter advancing, so
-inputs are in HBM when the timed region starts. Prints one JSON line.
+Every step, warm-up and timed, draws fresh seeded gradients first (Sec. 4: each training
+step takes a new batch); HIP events on the launch stream bracket each step's skew_step
+alone, so the draws are not timed and the inputs are resident in HBM when a step starts.
+The headline is the mean of the K timed steps. Prints one JSON line.
 
 Reported alongside the headline (parameters updated per second):
-  roofline      the dominant kernel's achieved algorithmic GB/s against 8 TB/s, from
-                HIP events recorded around each of the library's kernels on the launch
-                stream over the timed region; `traffic` from the committed rocprofv3
-                FETCH_SIZE / WRITE_SIZE summary when the kernel source still matches it
-  step          the whole step's algorithmic bytes and effective GB/s; the median, min and
-                max of the timed steps (an event between steps), and the warm-up steps
-                (steps 1.. of the run) timed one by one
-  cpu_baseline  the CPU oracle (plain C, OpenMP) on a bounded resident sample of the
-                same workload, on this host's cores
+  step          the step's algorithmic bytes (Table 6's state by tier: G read 2 B, W read and
+                written 4 B, fp32 momentum and exact V 8 B each per parameter) and its
+                effective GB/s and fraction of the 8 TB/s peak; median, min and max of the
+                timed steps; the warm-up steps (steps 1.. of the run) one by one
+  roofline      the dominant kernel's achieved algorithmic GB/s against 8 TB/s, from HIP
+                events around each of the library's kernels over a separate pass of steps
+                (so the headline's steps carry no per-kernel events); `traffic` from the
+                committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary when the kernel source
+                still matches it
+  tiers         per tier: parameters, algorithmic bytes, and the update kernel's measured
+                HBM bytes from the committed per-tier counter summary (same source check)
+  ceilings      a plain device copy of 2 GiB, timed in this process
+  cpu_baseline  the CPU oracle (plain C, OpenMP) over one whole step of the same workload
+                on this host's cores, and single-threaded on a sample (extrapolated)
 """
 from __future__ import annotations
 
@@ -42,6 +48,8 @@ BYTES_PER_PARAM = {"expert": 6, "backbone_matrix": 14, "backbone_vector": 22, "r
                    "expert_vector": 14, "router_vector": 14}
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_19058_amd", "csrc", "skew_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_full.json")
+TIER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_full_tiers.json")
+TIER_NAMES = {0: "backbone", 1: "expert", 2: "router"}
 
 
 def log(*a):
@@ -81,39 +89,123 @@ def kernel_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def cpu_baseline(wl, budget_s: float = 15.0) -> dict:
-    """The CPU oracle as it stands, on a resident sample of the workload: 8 expert
-    matrices, one attention matrix, one norm vector and one router, stepped repeatedly."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(wl, Wt, G, t: int, single_budget_s: float = 8.0) -> dict:
+    """The CPU oracle as it stands: one whole step over every tensor of the workload (the
+    weights and step-t gradients copied from the GPU, zero state) on this host's OpenMP
+    threads; then single-threaded on a sample of the workload's tensors, extrapolated."""
     import numpy as np
     import torch
     import oracle
-    from paper_2607_19058_amd import workloads as W
-    ex = [s for s in wl.specs if s.tier == W.EXPERT][:8]
-    bb = [s for s in wl.specs if s.tier == W.BACKBONE and len(s.shape) == 2 and s.shape == (2048, 2048)][:1]
-    vec = [s for s in wl.specs if s.tier == W.BACKBONE and len(s.shape) == 1][:1]
-    rt = [s for s in wl.specs if s.tier == W.ROUTER][:1]
-    sample = ex + bb + vec + rt
-    T = []
-    for s in sample:
-        w = W.init_weight(s, wl, "cpu").view(torch.int16).numpy().view(np.uint16).copy()
-        g = torch.empty(s.shape, dtype=torch.bfloat16)
-        W.fill_grad(s, wl, 1, g)
-        T.append(oracle.Tensor(tier=s.tier, w=w, g=g.view(torch.int16).numpy().view(np.uint16).copy(),
-                               tensor_id=s.tensor_id).init_state())
-    params = sum(s.numel for s in sample)
+
+    def host(x):
+        return x.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    T = [oracle.Tensor(tier=s.tier, w=host(Wt[k]), g=host(G[k]), tensor_id=s.tensor_id,
+                       state_flags=s.state_flags).init_state() for k, s in enumerate(wl.specs)]
+    params = sum(s.numel for s in wl.specs)
+    threads = oracle.threads()
     t0 = time.perf_counter()
-    steps = 0
-    while True:
-        steps += 1
-        oracle.step(T, steps)
-        if time.perf_counter() - t0 >= budget_s or steps >= 400:
-            break
+    oracle.step(T, t)
     dt = time.perf_counter() - t0
-    return {"value": round(params * steps / dt / 1e9, 4), "unit": "Gparams/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"{len(sample)} tensors of the full workload ({params:,} params: 8 expert matrices, "
-                      f"one 2048x2048 attention matrix, one norm vector, one router), {steps} steps, "
-                      f"{dt:.1f} s wall on {oracle.threads()} OpenMP threads"}
+    del T
+    # single thread: two expert matrices (both orientations), an attention matrix, a norm
+    # vector and a router, stepped until the budget is spent
+    from paper_2607_19058_amd import workloads as W
+    pick = []
+    for cond in (lambda s: s.tier == W.EXPERT and s.shape[0] < s.shape[-1],
+                 lambda s: s.tier == W.EXPERT and s.shape[0] > s.shape[-1],
+                 lambda s: s.tier == W.BACKBONE and len(s.shape) == 2 and s.shape[0] == s.shape[1],
+                 lambda s: s.tier == W.BACKBONE and len(s.shape) == 1,
+                 lambda s: s.tier == W.ROUTER):
+        ks = [k for k, s in enumerate(wl.specs) if cond(s)]
+        if ks:
+            pick.append(ks[0])
+    S = [oracle.Tensor(tier=wl.specs[k].tier, w=host(Wt[k]), g=host(G[k]), tensor_id=wl.specs[k].tensor_id,
+                       state_flags=wl.specs[k].state_flags).init_state() for k in pick]
+    sparams = sum(wl.specs[k].numel for k in pick)
+    oracle.set_threads(1)
+    try:
+        t1 = time.perf_counter()
+        steps = 0
+        while True:
+            steps += 1
+            oracle.step(S, t + steps - 1)
+            if time.perf_counter() - t1 >= single_budget_s or steps >= 50:
+                break
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_threads(threads)
+    one = sparams * steps / dt1 / 1e9
+    return {"value": round(params / dt / 1e9, 4), "unit": "Gparams/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": len(os.sched_getaffinity(0)),
+            "sample": f"one whole step of the workload ({len(wl.specs)} tensors, {params:,} params; weights and "
+                      f"step-{t} gradients copied from the GPU, zero state): {dt:.1f} s wall on {threads} OpenMP threads",
+            "single_thread": {"value": round(one, 4), "unit": "Gparams/s",
+                              "sample": f"{len(pick)} tensors ({sparams:,} params: "
+                                        + ", ".join(wl.specs[k].name for k in pick)
+                                        + f"), {steps} steps, {dt1:.1f} s on 1 thread",
+                              "extrapolated_all_cores": round(one * threads, 4),
+                              "note": "single-thread rate times the thread count: an extrapolation, not a measurement"}}
+
+
+def stream_ceilings(dev) -> dict:
+    """A plain device copy (read 2 GiB + write 2 GiB of bf16) with torch's own kernel, best
+    of 5: context for the step's rates."""
+    import torch
+    a = torch.ones(1 << 30, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    out = {}
+    for name, fn, nbytes in (("copy", lambda: b.copy_(a), 4 << 30),):
+        fn()
+        best = 1e30
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        out[f"{name}_GBps"] = round(nbytes / (best * 1e-3) / 1e9, 1)
+    out["note"] = "torch copy_ of 2 GiB of bf16 (2 GiB read + 2 GiB written), best of 5, in this process"
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
+def tier_table(wl) -> dict:
+    """Per tier: parameters and algorithmic bytes (Table 6's state by tier), with the update
+    kernel's measured HBM bytes from the committed per-tier counter summary when the kernel
+    source still matches it."""
+    measured = {}
+    if os.path.exists(TIER_TRAFFIC_FILE):
+        tr = json.load(open(TIER_TRAFFIC_FILE))
+        if tr.get("kernel_src_sha") == kernel_sha() and tr.get("workload") == wl.name:
+            measured = tr.get("tiers", {})
+    out = {}
+    for tier, name in TIER_NAMES.items():
+        specs = [s for s in wl.specs if s.tier == tier]
+        if not specs:
+            continue
+        params = sum(s.numel for s in specs)
+        alg = algorithmic_bytes(specs)
+        row = {"params": params, "algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3)}
+        m = measured.get(name)
+        if m:
+            row["p3_measured_bytes"] = m["hbm_bytes_per_launch"]
+            row["p3_measured_over_algorithmic"] = round(m["hbm_bytes_per_launch"] / alg, 4)
+        out[name] = row
+    return out
 
 
 def main() -> int:
@@ -123,7 +215,6 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="full")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--weight-decay", type=float, default=0.0,
                     help="decoupled weight decay lambda fused into the update (router exempt)")
     ap.add_argument("--max-grad-norm", type=float, default=0.0,
@@ -138,6 +229,11 @@ def main() -> int:
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run three plain 1 GiB device-to-device copies (read 1 GiB, write 1 GiB "
                          "each), whose FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures")
+    ap.add_argument("--tier", default="all", choices=["all", "backbone", "expert", "router"],
+                    help="only this tier's tensors of the workload (the per-tier traffic counters)")
+    ap.add_argument("--kernel-steps", type=int, default=5,
+                    help="steps of the separate pass that times each kernel with HIP events")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the in-process copy/read ceilings")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -163,10 +259,15 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
         log("[bench] calibration copies done (3 x 1 GiB)")
+    ceilings = None if args.no_ceilings else stream_ceilings(dev)
     wl = W.get(args.workload)
     if args.stacked:
         wl = W.stacked(wl)
     wl = W.with_variant(wl, args.variant)
+    if args.tier != "all":
+        import dataclasses
+        keep = {v: k for k, v in TIER_NAMES.items()}[args.tier]
+        wl = dataclasses.replace(wl, specs=[s for s in wl.specs if s.tier == keep])
     log(f"[bench] workload {wl.name}: {len(wl.specs)} tensors, {wl.numel:,} params; allocating")
     Wt = [W.init_weight(s, wl, dev) for s in wl.specs]
     G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
@@ -181,34 +282,40 @@ def main() -> int:
               weight_decay=args.weight_decay, max_grad_norm=args.max_grad_norm,
               flags=2 if args.exact_ulp else 0)
     stream = torch.cuda.current_stream()
-    first = []   # the warm-up steps (steps 1.. of the run) timed one by one, input drawing excluded
-    for t in range(1, args.warmup + 1):
-        draw(t)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        opt.step(t, **hp)
-        b.record(stream)
-        first.append((a, b))
-    draw(args.warmup + 1)
+
+    def steps(t_from, count):
+        """count steps from step t_from, each on a fresh draw; events bracket skew_step alone"""
+        ev = []
+        for t in range(t_from, t_from + count):
+            draw(t)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            opt.step(t, **hp)
+            b.record(stream)
+            ev.append((a, b))
+        return ev
+
+    first = steps(1, args.warmup)
     torch.cuda.synchronize()
     first_ms = [round(a.elapsed_time(b), 3) for a, b in first]
-    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps")
-
-    opt.timing_enable(args.steps)
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]   # one between steps
-    e0, e1 = evs[0], evs[-1]
+    log(f"[bench] warmup done ({args.warmup} steps); timing {args.steps} steps, fresh gradients each")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    e0.record(stream)
-    for j in range(args.steps):
-        opt.step(args.warmup + 1 + j, **hp)
-        evs[j + 1].record(stream)
+    timed = steps(args.warmup + 1, args.steps)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_ms = sorted(evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps))
+    step_ms = [a.elapsed_time(b) for a, b in timed]
+    ms_per_step = sum(step_ms) / len(step_ms)
+    step_sorted = sorted(step_ms)
+    # per-kernel times: a separate pass of steps with HIP events around each kernel
+    t_next = args.warmup + args.steps + 1
+    opt.timing_enable(args.kernel_steps)
+    steps(t_next, args.kernel_steps)
+    torch.cuda.synchronize()
     per_kernel = opt.timing_read()
     steps_rec = per_kernel.pop("_steps")
-    ev_ms = e0.elapsed_time(e1)
+    opt.timing_enable(0)
+    t_last = t_next + args.kernel_steps - 1
     unfused_ms = None
     if args.max_grad_norm > 0:
         # what the fused scaling replaces: torch's clip_grad_norm_ on the same bf16 gradients
@@ -232,7 +339,6 @@ def main() -> int:
         unfused_ms = c0.elapsed_time(c1) / 3
         del Gc
 
-    ms_per_step = 1e3 * wall / args.steps
     params = wl.numel
     alg = algorithmic_bytes(wl.specs)
     kern_avg = {k: v / max(1, steps_rec) for k, v in per_kernel.items()}
@@ -263,27 +369,33 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
+        "achieved_GBps": round(step_gbps, 1),
+        "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),
         "config": {"workload": f"{wl.name}: {params:,}-parameter synthetic MoE parameter set, {len(wl.specs)} tensors "
-                               "(bf16 weights and gradients, fp32 state)",
+                               "(bf16 weights and gradients, fp32 state)"
+                               + ("" if args.tier == "all" else f", {args.tier} tier only"),
                    "params": params, "tensors": len(wl.specs), "state_bytes": opt.state_nbytes,
                    "workspace_bytes": opt.workspace_nbytes, "weight_decay": args.weight_decay,
                    "max_grad_norm": args.max_grad_norm, "variant": args.variant, "stacked": args.stacked,
-                   "exact_ulp": args.exact_ulp},
+                   "exact_ulp": args.exact_ulp, "tier": args.tier,
+                   "gradients": "fresh seeded draw before every step (not timed)"},
         "roofline": roof,
         "step": {"algorithmic_bytes": alg, "bytes_per_param": round(alg / params, 3),
                  "effective_GBps": round(step_gbps, 1), "frac_of_peak": round(step_gbps / PEAK_GBPS, 4),
-                 "event_ms_per_step": round(ev_ms / args.steps, 4),
-                 "ms_median": round(step_ms[len(step_ms) // 2], 4), "ms_min": round(step_ms[0], 4),
-                 "ms_max": round(step_ms[-1], 4),
+                 "ms_mean": round(ms_per_step, 4), "ms_median": round(step_sorted[len(step_sorted) // 2], 4),
+                 "ms_min": round(step_sorted[0], 4), "ms_max": round(step_sorted[-1], 4),
+                 "wall_ms_per_step_with_draws": round(1e3 * wall / args.steps, 4),
                  "warmup_steps_ms": first_ms,   # steps 1.. of the run, before the timed region
-                 "kernel_ms_per_step": {k: round(v, 4) for k, v in kern_avg.items()}},
+                 "kernel_ms_per_step": {k: round(v, 4) for k, v in kern_avg.items()},
+                 "kernel_pass_steps": steps_rec},
+        "tiers": tier_table(wl),
+        **({"ceilings": ceilings} if ceilings else {}),
         **({"torch_clip_grad_norm_ms": round(unfused_ms, 4)} if unfused_ms is not None else {}),
     }
     if not args.no_cpu_baseline:
-        del Wt, G, opt
-        torch.cuda.empty_cache()
-        log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        del opt
+        log("[bench] timing the CPU oracle: one whole step, then single-threaded on a sample")
+        out["cpu_baseline"] = cpu_baseline(wl, Wt, G, t_last)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -219,7 +219,7 @@ int init_ctx(skew_ctx **ctx, Plan &p, skew_tensor_desc *d, int n, void *state, s
   std::vector<Item> zv[kZVariants];
   for (const Item &it : p.z) {
     const DevTensor &x = table[it.tensor];
-    const int lg = x.nseg == 1 ? 0 : (x.nseg == 2 ? 1 : 2);
+    const int lg = x.nseg == 1 ? 0 : (x.nseg == 2 ? 1 : (x.nseg == 4 ? 2 : 3));
     zv[lg * 4 + (x.vec ? 0 : 2) + (x.momentum ? 1 : 0)].push_back(it);
   }
   skew_ctx *c = new (std::nothrow) skew_ctx;

@@ -27,7 +27,8 @@ constexpr int kZMaxSeg = 4;              // 512-column chunks per wave and row
 constexpr int64_t kZBandElems = 1 << 21; // elements per row band, at most: 4 MiB of bf16 gradient
 constexpr int64_t kZMinBandElems = 1 << 19;   // ... and at least (unless a row is longer)
 constexpr double kZTargetBands = 1024.0;      // bands per row-band launch class, about
-constexpr int kZVariants = 12;           // kernel variants: log2(nseg) * 4 + (element loads ? 2 : 0) + momentum
+constexpr int kZVariants = 16;           // kernel variants: lg(nseg) * 4 + (element loads ? 2 : 0) + momentum,
+                                         // lg = 0, 1, 2, 3 for nseg = 1, 2, 4, 3 (3: no momentum)
 constexpr int kZLdsBytes = 64 * 1024;    // one LDS staging buffer of the row-band pass (two per work-group)
 constexpr int kZMaxBlockRows = 64;       // rows staged per block, at most
 constexpr int kZMaxBandRows = 2048;      // rows per band, at most (their R are staged in LDS)
@@ -84,13 +85,15 @@ struct BandStats {
   int32_t pad;
 };
 
-// Per fold chunk of columns of a row-band tensor.
+// Per fold chunk of columns of a row-band tensor (of a wide factored tensor: per fold chunk of
+// rows, then of columns, only cmin, cmax and cdup: extremes and equal neighbours of R or C).
 struct ColStats {
   double s;       // sum over the chunk's columns of z_j / c'_j (U_hat^2 summed above the floor)
   float cmin;     // min c'_j over columns with C_j > 0 (+inf if none)
   float cmax;     // max c'_j
   int32_t bad;    // non-finite c'_j, or C_j == 0 with a nonzero column sum
   int32_t cdup;   // columns whose C_j > 0 equals the previous column's within the chunk
+  double s2;      // sum over the chunk's columns of z_j / c'_j^2 (bounds the sum of squared terms)
 };
 
 // Device-resident description of one tensor, its state and its partial sums.
@@ -105,7 +108,8 @@ struct DevTensor {
                           //            tensors: [ceil(n / kFold)], in the gradient-norm mode)
   double *zpart;          // [nzb][m]   row-band pass: partial column sums of (s x)^2 / R_i
   BandStats *bst;         // [nzb]      row-band pass: per band
-  ColStats *cst;          // [nfc]      row-band pass: per fold chunk of columns
+  ColStats *cst;          // [nfc]      row-band pass: per fold chunk of columns; wide factored
+                          //            tensors: [nfr + nfc] extremes and equal neighbours of R, C
   double *ssum;           // [ntr*ntc]  per-tile sums of squares of the unclipped update
   double *qsum;           // [ntr*ntc]  per-tile sums of U_hat^4 over the approximated elements
   TensorScalars *sc;      // this step's clip factor and reconstruction clamp
@@ -119,7 +123,7 @@ struct DevTensor {
   int32_t momentum;       // backbone tier
   int32_t vec;            // 16-byte aligned rows: vector loads and stores
   int32_t zpath;          // 1: pass 1 is the row-band pass (no separate update-sum pass)
-  int32_t nseg;           // row-band pass: 512-column chunks per wave (1..kZMaxSeg)
+  int32_t nseg;           // row-band pass: 512-column chunks per wave (1, 2, 3 or 4)
   int32_t zcw;            // row-band pass: 512-column chunks per row
   int32_t zrpi;           // row-band pass: row groups per work-group (rows side by side); a group
                           // is wpr = ceil(zcw / nseg) waves, wave w of it takes chunks w, w + wpr
@@ -205,7 +209,7 @@ constexpr size_t static_workspace_bytes() { return (size_t)SKEW_STATIC_WORKSPACE
 
 // Kernel launchers (skew_kernels.hip). Return a hipError_t value.
 int launch_p1(const DevTensor *T, const Item *items, int64_t count, void *stream);
-// row-band pass, kernel variant log2(nseg) * 4 + (element loads ? 2 : 0) + (momentum ? 1 : 0)
+// row-band pass, kernel variant lg(nseg) * 4 + (element loads ? 2 : 0) + (momentum ? 1 : 0)
 // mode 0: the whole pass; 1: sums of g^2 only (row sums to ainv); 2: z, floored sum and
 // band statistics from the R already folded (the gradient-norm mode's two passes)
 int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, int variant, int mode,

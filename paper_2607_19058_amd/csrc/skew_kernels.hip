@@ -713,8 +713,8 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // the compiler holds (and spills).
   constexpr int RBB = (8 / NSEG < RB ? 8 / NSEG : RB) > 0 ? (8 / NSEG < RB ? 8 / NSEG : RB) : 1;
   // the block's staged gradient stays in registers from the first sweep to the second where
-  // it fits (no momentum, up to two chunks per wave; the other variants would spill)
-  constexpr bool KEEP = !MOM && NSEG <= 2;
+  // it fits (no momentum, up to three chunks per wave; the other variants would spill)
+  constexpr bool KEEP = !MOM && NSEG <= 3;
   auto read_rows = [&](const unsigned char *buf, int b0, uint4 (&uk)[RB][NSEG]) {
     const unsigned char *ptr[RBB * NSEG];
 #pragma unroll
@@ -1004,12 +1004,12 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   const int mode = GN ? mode_arg : 0;
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
-  // rows per group and block: the planner keeps 4 at most with one or two chunks per wave
-  // and 1 with four, which keeps every variant's loop free of register spills
+  // rows per group and block: the planner keeps 4 at most with one or two chunks per wave,
+  // 2 with three and 1 with four, which keeps every variant's loop free of register spills
   if (NSEG <= 2 && t.zrb >= 4)
     p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
-  else if (NSEG <= 2 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 2 ? 2 : 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+  else if (NSEG <= 3 && t.zrb >= 2)
+    p1z_body<NSEG, NSEG <= 3 ? 2 : 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else
     p1z_body<NSEG, 1, MOM, VEC, GN>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
 }
@@ -1066,6 +1066,23 @@ __device__ __forceinline__ float mean_r_clamped(const DevTensor &t, const StepCo
   return mean_r_of(t, k, RedGroup{sh});
 }
 
+// Extremes of the positive values and equal neighbours within one fold chunk (v of this
+// thread's row or column, 0 past the end), for the clip stage's test of repeated factors;
+// every thread of the work-group calls it
+__device__ __forceinline__ void chunk_repeats(ColStats *out, float v, float *nb, double *sh) {
+  nb[threadIdx.x] = v;
+  __syncthreads();
+  const double dup = (threadIdx.x > 0 && v > 0.f && v == nb[threadIdx.x - 1]) ? 1.0 : 0.0;
+  const double d = block_sum(dup, sh);
+  const float mn = wg_min_wf<kWaves>(v > 0.f ? v : __builtin_inff(), sh);
+  const float mx = wg_max_wf<kWaves>(v, sh);
+  if (threadIdx.x == 0) {
+    stg(&out->cmin, mn);
+    stg(&out->cmax, mx);
+    stg(&out->cdup, (int32_t)d);
+  }
+}
+
 // --------------------------------------------------------------------------------------------
 // fold: R_i <- b2 R_i + a2 r_i, C_j <- b2 C_j + a2 c_j (Eq. 1), 1/sqrt(R_i), sums of R
 // --------------------------------------------------------------------------------------------
@@ -1080,9 +1097,11 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
   // where their row sums of g^2 wait in ainv
   const int nrows = t.zpath ? (phase == 1 ? (int)((t.n + kFold - 1) / kFold) : 0) : t.nfr;
   if (phase == 2 && !t.zpath) return;
+  __shared__ float nb[kThreads];
   if (it.tile < nrows) {
     const int64_t i = (int64_t)it.tile * kFold + threadIdx.x;
     double rn = 0.0;
+    float Rv = 0.f;
     if (i < t.n) {
       double s = 0.0;
       if (t.zpath)
@@ -1095,27 +1114,32 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
       stg(t.R + i, R);
       stg(t.ainv + i, 1.0 / sqrt((double)R));
       rn = (double)R;
+      Rv = R;
     }
     const double tot = block_sum(rn, sh);
     if (threadIdx.x == 0) stg(t.rsum + it.tile, tot);
+    if (!t.zpath) chunk_repeats(t.cst + it.tile, Rv, nb, sh);
   } else if (!t.zpath || phase == 1) {
     // C_j from the column partials ([row bands][m] of either pass 1)
     const int64_t j = (int64_t)(it.tile - nrows) * kFold + threadIdx.x;
+    float Cv = 0.f;
     if (j < t.m) {
       double s = 0.0;
       const int nb = t.zpath ? t.nzb : t.ntr;
 #pragma unroll 8
       for (int b = 0; b < nb; b++) s += ldg(t.colpart + (int64_t)b * t.m + j);
       const float cj = (float)((phase == 1 ? c2 * s : s) / (double)t.n);
-      stg(t.C + j, fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j))));
+      Cv = fmaf(k.a2, cj, __fmul_rn(k.b2, ldg(t.C + j)));
+      stg(t.C + j, Cv);
     }
+    if (!t.zpath) chunk_repeats(t.cst + t.nfr + (it.tile - nrows), Cv, nb, sh);
   } else {
     // row-band tensor: C_j (phase 0; phase 2 has it from phase 1), c'_j = C_j / max(mean R,
     // eps) and sum_j z_j / c'_j over the chunk
     __shared__ float cprev[kThreads];
     const float q = mean_r_clamped(t, k, sh);
     const int64_t j = (int64_t)it.tile * kFold + threadIdx.x;
-    double sj = 0.0;
+    double sj = 0.0, sj2 = 0.0;
     float cmn = __builtin_inff(), cmx = 0.f, Cj = 0.f;
     int bad = 0;
     if (j < t.m) {
@@ -1140,6 +1164,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
         // c'_j that is zero or not finite leaves the tensor to the exact pass
         if (cp > 0.f && cp < __builtin_inff()) {
           sj = zs / (double)cp;
+          sj2 = sj / (double)cp;
           cmn = cmx = cp;
         } else {
           bad = 1;
@@ -1153,12 +1178,14 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const DevTensor *__restr
     __syncthreads();
     const double dup = (threadIdx.x > 0 && Cj > 0.f && Cj == cprev[threadIdx.x - 1]) ? 1.0 : 0.0;
     const double S = block_sum(sj, sh);
+    const double S2 = block_sum(sj2, sh);
     const double cdup = block_sum(dup, sh);
     const float cmin = wg_min_wf<kWaves>(cmn, sh);
     const float cmax = wg_max_wf<kWaves>(cmx, sh);
     const int b = wg_or_w<kWaves>(bad, sh);
     if (threadIdx.x == 0) {
       stg(&t.cst[it.tile].cdup, (int32_t)cdup);
+      stg(&t.cst[it.tile].s2, S2);
       stg(&t.cst[it.tile].s, S);
       stg(&t.cst[it.tile].cmin, cmin);
       stg(&t.cst[it.tile].cmax, cmax);
@@ -1642,23 +1669,25 @@ __device__ __forceinline__ int repeats_rule(const DevTensor &t, float rmn, float
   const bool uc = t.m > 1 && cmx <= cmn * (1.f + 0x1p-20f);
   return (ur || uc || 64.0 * dup_r > (double)t.n || 64.0 * dup_c > (double)t.m) ? 1 : 0;
 }
-// wide factored tensors: a scan of R and C (the row-band tensors have these in their band
-// and column-chunk statistics)
+// wide factored tensors: from the fold's per-chunk statistics of R and C (the row-band
+// tensors have these in their band and column-chunk statistics)
 template <class Red>
 __device__ __forceinline__ int repeated_factors(const DevTensor &t, const Red &r) {
   double dup_r = 0.0, dup_c = 0.0;
   float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
-  for (int64_t i = r.lane(); i < t.n; i += Red::kN) {
-    const float a = ldg(t.R + i);
-    if (i > 0 && a > 0.f && a == ldg(t.R + i - 1)) dup_r += 1.0;
-    if (a > 0.f) rmn = fminf(rmn, a);
-    rmx = fmaxf(rmx, a);
-  }
-  for (int64_t j = r.lane(); j < t.m; j += Red::kN) {
-    const float a = ldg(t.C + j);
-    if (j > 0 && a > 0.f && a == ldg(t.C + j - 1)) dup_c += 1.0;
-    if (a > 0.f) cmn = fminf(cmn, a);
-    cmx = fmaxf(cmx, a);
+  for (int64_t q = r.lane(); q < (int64_t)t.nfr + t.nfc; q += Red::kN) {
+    const ColStats *c = t.cst + q;
+    const float mn = ldg(&c->cmin), mx = ldg(&c->cmax);
+    const double d = (double)ldg(&c->cdup);
+    if (q < t.nfr) {
+      rmn = fminf(rmn, mn);
+      rmx = fmaxf(rmx, mx);
+      dup_r += d;
+    } else {
+      cmn = fminf(cmn, mn);
+      cmx = fmaxf(cmx, mx);
+      dup_c += d;
+    }
   }
   dup_r = r.sum(dup_r);
   dup_c = r.sum(dup_c);
@@ -1678,6 +1707,8 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
     const int64_t bstride = sizeof(BandStats) / sizeof(double), cstride = sizeof(ColStats) / sizeof(double);
     const double Y = red_sum(r, &t.bst->ysum, t.nzb, bstride);
     const double SU = red_sum(r, &t.cst->s, t.nfc, cstride);
+    // sum over the terms t_ij = (s x)^2 / (R_i c'_j) of t_ij^2 <= umax * sum_j z_j / c'_j^2
+    const double SU2 = red_sum(r, &t.cst->s2, t.nfc, cstride);
     double um = 0.0, dup_r = 0.0, dup_c = 0.0;
     float rmn = __builtin_inff(), rmx = 0.f, cmn = __builtin_inff(), cmx = 0.f;
     int bad = 0;
@@ -1714,7 +1745,7 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
       o.S = SU;
     } else if (have_z && lo >= k.eps) {   // nothing on the floor
       o.S = SU;
-      o.E = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um / (double)cmn * SU) + 1e-14 * SU : 0.0;
+      o.E = SU > 0.0 ? 20.0 * 0x1p-23 * sqrt(um * SU2) + 1e-14 * SU : 0.0;
       if (o.repeats) o.E = fmax(o.E, kRigorousRel * SU + 1e-14 * SU);
     } else if (have_y && hi < k.eps) {    // everything on the floor
       o.S = Y;
@@ -2133,6 +2164,8 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
     SKEW_P1Z_CASE(9, 4, true, true)
     SKEW_P1Z_CASE(10, 4, false, false)
     SKEW_P1Z_CASE(11, 4, false, true)
+    SKEW_P1Z_CASE(12, 3, true, false)
+    SKEW_P1Z_CASE(14, 3, false, false)
 #undef SKEW_P1Z_CASE
     default: return (int)hipErrorInvalidValue;
   }

@@ -13,8 +13,10 @@ namespace skew {
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Row-band pass for factored matrices whose staged rows fit: zcw 512-column chunks per
-// row, nseg (1, 2 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
-// row and rpi = 8 / wpr rows are side by side. A block of rpi * zrb rows (bf16 gradient,
+// row, nseg (1, 2, 3 or 4) of them per wave, so wpr = ceil(zcw / nseg) <= 8 waves share a
+// row and rpi = 8 / wpr rows are side by side. Three chunks per wave (rows of 8193 to
+// 12288 columns, e.g. 11008) keep the lean loads and the block in registers; they are
+// used without momentum only (with it, the general loop's four chunks per wave). A block of rpi * zrb rows (bf16 gradient,
 // plus fp32 momentum on the backbone) fills at most one LDS buffer. zrb = 0: no row band.
 struct RowBandShape {
   int64_t zcw, nseg, rpi, zrb;
@@ -22,11 +24,12 @@ struct RowBandShape {
 static RowBandShape rowband_shape(int64_t m, bool momentum) {
   RowBandShape r;
   r.zcw = ceil_div(m, kChunk);
-  r.nseg = r.zcw <= 1 ? 1 : (r.zcw <= 2 * kZWaves ? 2 : 4);
+  r.nseg = r.zcw <= 1 ? 1 : (r.zcw <= 2 * kZWaves ? 2 : (!momentum && r.zcw <= 3 * kZWaves ? 3 : 4));
   const int64_t wpr = ceil_div(r.zcw, r.nseg);
   const int64_t row_kb = r.zcw * (momentum ? 3 : 1);   // staged KiB per row
   r.rpi = wpr <= kZWaves ? kZWaves / wpr : 0;
-  r.zrb = r.rpi > 0 ? std::min<int64_t>(r.nseg <= 2 ? 4 : 1, kZLdsBytes / (r.rpi * row_kb * 1024)) : 0;
+  r.zrb = r.rpi > 0 ? std::min<int64_t>(r.nseg <= 2 ? 4 : (r.nseg == 3 ? 2 : 1), kZLdsBytes / (r.rpi * row_kb * 1024))
+                    : 0;
   while (r.zrb & (r.zrb - 1)) r.zrb &= r.zrb - 1;   // a power of two: 1, 2 or 4
   return r;
 }
@@ -191,6 +194,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
       tp.off_colpart = ws_part; ws_part = align_up(ws_part + (size_t)ntr * tp.m * 8);
       tp.off_ainv = ws_part; ws_part = align_up(ws_part + (size_t)tp.n * 8);
       tp.off_rsum = ws_part; ws_part = align_up(ws_part + (size_t)nfr * 8);
+      tp.off_cst = ws_part; ws_part = align_up(ws_part + (size_t)(nfr + nfc) * sizeof(ColStats));
       for (int32_t k = 0; k < tp.ntr * tp.ntc; k++) p.p1.push_back({i, k});
       for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold.push_back({i, k});
       for (int32_t k = 0; k < tp.nfr + tp.nfc; k++) p.fold_rows.push_back({i, k});

@@ -107,7 +107,7 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
   check_items(mode == 0 ? "z0" : (mode == 1 ? "z1" : "z2"), T, items, count);
   for (int64_t q = 0; q < count; q++) {
     const DevTensor &t = T[items[q].tensor];
-    const int lg = t.nseg == 1 ? 0 : (t.nseg == 2 ? 1 : 2);
+    const int lg = t.nseg == 1 ? 0 : (t.nseg == 2 ? 1 : (t.nseg == 4 ? 2 : 3));
     CHECK(variant == lg * 4 + (t.vec ? 0 : 2) + (t.momentum ? 1 : 0), "row-band variant %d", variant);
   }
   return 0;
@@ -232,6 +232,8 @@ static void check_plan(const std::string &name, const std::vector<skew_tensor_de
             "%s: chunk layout zcw %d nseg %d rpi %d", tn.c_str(), tp.zcw, tp.nseg, tp.zrpi);
       const int64_t block_bytes = blk * tp.zcw * 1024 * (tp.momentum ? 3 : 1);
       CHECK(block_bytes <= kZLdsBytes, "%s: block of %lld bytes", tn.c_str(), (long long)block_bytes);
+      CHECK(tp.nseg != 3 || (!tp.momentum && tp.zrb <= 2), "%s: three chunks per wave without momentum, 2 rows",
+            tn.c_str());
       for (int b = 0; b < tp.nzb; b++) {
         CHECK(z.count({i, b}) == 1, "%s: band %d", tn.c_str(), b);
         n_z++;
@@ -255,6 +257,7 @@ static void check_plan(const std::string &name, const std::vector<skew_tensor_de
       ws.push_back({tp.off_colpart, tp.off_colpart + (size_t)tp.ntr * tp.m * 8, tn + ".colpart"});
       ws.push_back({tp.off_ainv, tp.off_ainv + (size_t)tp.n * 8, tn + ".ainv"});
       ws.push_back({tp.off_rsum, tp.off_rsum + (size_t)tp.nfr * 8, tn + ".rsum"});
+      ws.push_back({tp.off_cst, tp.off_cst + (size_t)(tp.nfr + tp.nfc) * sizeof(ColStats), tn + ".cst"});
     }
     if (!tp.zpath)
       for (int64_t k = 0; k < tiles * kSub; k++) {

@@ -67,15 +67,59 @@ def test_key_depends_on_every_input():
     assert base not in others and len(others) == 3
 
 
-def test_u16_range_and_pairing():
-    key = oracle.dither_key(3, 5, 11)
-    u = oracle.dither_u16(key, 0, 1 << 12)
-    assert u.max() < 65536
-    # elements 2p and 2p+1 take the two halves of one 32-bit hash of p
-    h = np.array([oracle.fmix32((p ^ (key & 0xFFFFFFFF) ^ oracle.fmix32(key >> 32)) & 0xFFFFFFFF)
-                  for p in range(1 << 11)], np.uint64)
-    assert np.array_equal(u[0::2], (h & 0xFFFF).astype(np.uint32))
-    assert np.array_equal(u[1::2], (h >> 16).astype(np.uint32))
+def _published():
+    """(function, input) -> output of the published mixer vectors in tests/golden."""
+    out = {}
+    for line in open(os.path.join(GOLD, "hash_vectors.txt")):
+        line = line.split("|")[0].strip()
+        if line and not line.startswith("#"):
+            fn, x, y = line.split()
+            out[(fn, int(x, 16))] = int(y, 16)
+    return out
+
+
+def _i64(u):
+    return u - (1 << 64) if u >= 1 << 63 else u
+
+
+def test_key_composition_against_published_outputs():
+    """K = mix64(mix64(mix64(seed) ^ t) ^ tensor_id), pinned without re-computing a mixer: with
+    seed = SplitMix64's first state, t and tensor_id chosen so that each argument is the next
+    state, K must be SplitMix64's third published output (a different order or a dropped xor
+    would land on unpublished inputs)."""
+    P = _published()
+    s1, s2, s3 = 0x9E3779B97F4A7C15, 0x3C6EF372FE94F82A, 0xDAA66D2C7DDF743F
+    o1, o2, o3 = P[("mix64", s1)], P[("mix64", s2)], P[("mix64", s3)]
+    t = o1 ^ s2
+    tid = o2 ^ s3
+    assert oracle.dither_key(s1, _i64(t), tid) == o3
+
+
+def test_u16_composition_against_published_outputs():
+    """u16 of element idx: h = fmix32(lo(p) ^ lo(K) ^ fmix32(hi(p) ^ hi(K))) for the pair p =
+    idx >> 1; the even element takes h's low 16 bits, the odd one its high 16 bits. Pinned by
+    choosing p and K so that every fmix32 argument is an input of a published MurmurHash3 vector
+    (fmix32(0) = 0, fmix32(1) = 0x514E28B7, fmix32(0xFFFFFFFF) = 0x81F16F39)."""
+    P = _published()
+    f0, f1, fm = P[("fmix32", 0)], P[("fmix32", 1)], P[("fmix32", 0xFFFFFFFF)]
+    K = P[("mix64", 0xDAA66D2C7DDF743F)]   # a published 64-bit key (the key of the test above)
+    klo, khi = K & 0xFFFFFFFF, K >> 32
+
+    def u(p, odd):
+        return int(oracle.dither_u16(K, 2 * p + odd, 1)[0])
+
+    cases = []
+    # hi(p) = hi(K): the inner term is fmix32(0) = 0, so h = fmix32(lo(p) ^ lo(K))
+    for arg, h in ((1, f1), (0xFFFFFFFF, fm), (0, f0)):
+        cases.append(((khi << 32) | (klo ^ arg), h))
+    # hi(p) ^ hi(K) = 1: the inner term is fmix32(1); it cancels against lo(p)
+    inner = f1
+    for arg, h in ((1, f1), (0xFFFFFFFF, fm), (0, f0)):
+        cases.append((((khi ^ 1) << 32) | (klo ^ inner ^ arg), h))
+    for p, h in cases:
+        assert u(p, 0) == h & 0xFFFF, (hex(p), hex(h))
+        assert u(p, 1) == h >> 16, (hex(p), hex(h))
+    assert oracle.dither_u16(K, 0, 1 << 12).max() < 65536
 
 
 def _chi2_p(counts):

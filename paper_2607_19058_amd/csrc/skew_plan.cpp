@@ -139,8 +139,16 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     }
 
     // tile grid: tr rows x (512 * cw) columns, about kTileElems elements; cw in {1, 2, 4}
-    // so that the four waves of a work-group map onto (chunk, row) pairs statically
+    // so that the four waves of a work-group map onto (chunk, row) pairs statically. The widest
+    // strip that fits; a narrower one when the last strip would leave more than 1/16 of the
+    // row's width in idle lanes (1536 columns: 512 of 2048; 11008: 1280 of 12288)
     tp.cw = tp.m > 2 * kChunk ? 4 : (tp.m > kChunk ? 2 : 1);
+    {
+      auto waste = [&](int64_t cw) { return ceil_div(tp.m, (int64_t)kChunk * cw) * kChunk * cw - tp.m; };
+      if (16 * waste(tp.cw) > tp.m)
+        for (int32_t cw = tp.cw / 2; cw >= 1; cw /= 2)
+          if (waste(cw) < waste(tp.cw)) tp.cw = cw;
+    }
     const int64_t tc = (int64_t)kChunk * tp.cw;
     // (exact-moment tensors take a quarter of that: their element-by-element path is the
     // slowest per element, and their few tiles would otherwise finish last)

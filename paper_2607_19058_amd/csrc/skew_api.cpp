@@ -215,12 +215,16 @@ int init_ctx(skew_ctx **ctx, Plan &p, skew_tensor_desc *d, int n, void *state, s
     x.tensor_id = dd.tensor_id;
   }
   // row-band pass items by kernel variant (16-byte aligned rows or element loads is known
-  // only here, from the pointers)
+  // only here, from the pointers). The aligned variants without momentum and up to two
+  // chunks per wave address a block of rows by 32-bit byte offsets; a row stride that makes a
+  // block span 2^31 bytes or more takes the element-load variant instead.
   std::vector<Item> zv[kZVariants];
   for (const Item &it : p.z) {
     const DevTensor &x = table[it.tensor];
     const int lg = x.nseg == 1 ? 0 : (x.nseg == 2 ? 1 : (x.nseg == 4 ? 2 : 3));
-    zv[lg * 4 + (x.vec ? 0 : 2) + (x.momentum ? 1 : 0)].push_back(it);
+    const bool wide_span = (int64_t)x.zrpi * x.zrb * x.ld * 2 > 0x7FFFFFFF;
+    const bool vec = x.vec && !(wide_span && !x.momentum && x.nseg <= 2);
+    zv[lg * 4 + (vec ? 0 : 2) + (x.momentum ? 1 : 0)].push_back(it);
   }
   skew_ctx *c = new (std::nothrow) skew_ctx;
   if (c == nullptr) return SKEW_ENOMEM;

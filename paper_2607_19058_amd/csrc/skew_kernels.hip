@@ -558,6 +558,12 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
+  // Register staging (aligned rows, no momentum, up to two chunks per wave, the normal
+  // step): each wave loads its own pieces of the next block straight into registers by
+  // buffer loads while it sums the current one. Lanes past the row's end and rows past the
+  // band's end take an offset beyond the buffer's range, so the hardware returns zeros for
+  // them. The planner keeps a block's byte span below 2^31 for these tensors.
+  constexpr bool REG = VEC && !MOM && !GN && NSEG <= 2;
   const int wpr = (zcw + NSEG - 1) / NSEG;   // waves per row
   const int grp = wave / wpr;
   const int wg = wave - grp * wpr;           // wave within the group
@@ -616,7 +622,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // (read once, not per piece). With momentum, the fp32 row of M follows in two 1 KiB halves
   // per piece (masks cm0, cm1). The momentum variants with four chunks per wave or in the
   // gradient-norm passes keep the general loop: the registers of the lean one would spill.
-  constexpr bool LEAN = VEC && (!MOM || (NSEG <= 2 && !GN));
+  constexpr bool LEAN = !REG && VEC && (!MOM || (NSEG <= 2 && !GN));
   uint32_t cmask = 0, cm0 = 0, cm1 = 0;
   const uint16_t *gptr = t.g, *zptr = t.zeros;
   const float *mptr = t.M, *rptr = t.R;
@@ -704,6 +710,33 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         rbuf[lane] = ldg(t.R + ic);
     }
   };
+  // register staging: byte offsets of the lane's pieces from the block's first row (the
+  // sentinel 2^31 lies beyond any block's range), the block's buffer descriptor, and the old
+  // R of the row whose fold the lane takes part in (lane b * P + w: row b of its group)
+  uint32_t vo[RB][NSEG];
+  const int rfold = grp_c * RB + ((lane / P) < RB ? (lane / P) : 0);
+  if constexpr (REG) {
+#pragma unroll
+    for (int b = 0; b < RB; b++)
+#pragma unroll
+      for (int s = 0; s < NSEG; s++)
+        vo[b][s] = sok[s] ? (uint32_t)((((int64_t)grp_c * RB + b) * ld + col[s]) * 2) : 0x80000000u;
+  }
+  auto issue_reg = [&](int64_t blk, uint4 (&dst)[RB][NSEG], float &rold) {
+    const int64_t rbase = r0 + blk * br;
+    const int64_t span = (r1 - rbase) * ld * 2;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(t.g + rbase * ld), (short)0, (int)(span < 0x7FFFFFFF ? span : 0x7FFFFFFF), 0x00020000);
+#pragma unroll
+    for (int b = 0; b < RB; b++)
+#pragma unroll
+      for (int s = 0; s < NSEG; s++) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[b][s], 0, 0);
+        dst[b][s] = make_uint4(v.x, v.y, v.z, v.w);
+      }
+    const int64_t i = rbase + rfold;
+    rold = ldg(t.R + (i < r1 ? i : r1 - 1));
+  };
   // The lane's NSEG pieces of RB block rows are read from LDS in batches of RBB rows into
   // uk[b0 .. b0 + RBB). Staged padding is zero; a segment past the row's last chunk
   // (wave-uniform) reads the buffer's zero area instead. Every address lies in the buffer
@@ -738,10 +771,17 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         for (int s = 0; s < NSEG; s++) uk[b0 + b][s] = u[b * NSEG + s];
     }
   };
-  auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt) {
-    __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
-    __builtin_amdgcn_s_barrier();               // ... by every wave; the other buffer is free
-    if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
+  auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt,
+                  uint4 (&regc)[RB][NSEG], float rold, uint4 (&regn)[RB][NSEG], float &rnold) {
+    if constexpr (REG) {
+      // the next block's loads go out first; the compiler waits for this block's registers
+      // where they are first used
+      if (blk + 1 < nblk) issue_reg(blk + 1, regn, rnold);
+    } else {
+      __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);   // this block's loads (issued one block earlier)
+      __builtin_amdgcn_s_barrier();               // ... by every wave; the other buffer is free
+      if (blk + 1 < nblk) issue(blk + 1, nxt, rnxt);
+    }
     const int64_t rbase = r0 + blk * br;
     double *slot = rowsh + (blk & 1) * kZRowSlots;   // [block row][wave in group]
     // the lane's staged gradient of the block (the second sweep reads it again unless KEEP)
@@ -752,7 +792,14 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       double rp[RB];
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
-        read_rows(cur, b0, uk);
+        if constexpr (REG) {
+#pragma unroll
+          for (int bb = 0; bb < RBB; bb++)
+#pragma unroll
+            for (int s = 0; s < NSEG; s++) uk[b0 + bb][s] = regc[b0 + bb][s];
+        } else {
+          read_rows(cur, b0, uk);
+        }
 #pragma unroll
         for (int bb = 0; bb < RBB; bb++) {
           const int b = b0 + bb;
@@ -819,7 +866,8 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
         }
       } else {
       const float ri = div_to_float(x, dm, rdm);
-      const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, rcur[r]));
+      const float Rold = REG ? rold : rcur[r];   // (REG: the lane's row is r)
+      const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, Rold));
       const double Rd = (double)R;
       const bool normal = R > 0.f && R < __builtin_inff();
       winv_l = (R > 0.f && i < r1) ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
@@ -836,7 +884,22 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       constexpr bool Z = decltype(zc)::value, Y = decltype(yc)::value;
 #pragma unroll
       for (int b0 = 0; b0 < RB; b0 += RBB) {
-      if (!KEEP || mode == 2) read_rows(cur, b0, uk);   // (mode 2: the first sweep did not run)
+      if constexpr (!REG) {
+        if (!KEEP || mode == 2) read_rows(cur, b0, uk);   // (mode 2: the first sweep did not run)
+      } else {
+        // the packed block is unpacked again here (in place: the registers are not needed
+        // after this sweep); keeping sweep 1's floats beside the next block's registers would
+        // spill
+#pragma unroll
+        for (int bb = 0; bb < RBB; bb++)
+#pragma unroll
+          for (int s = 0; s < NSEG; s++) {
+            const uint4 &q = regc[b0 + bb][s];
+            u32x4_t v = {q.x, q.y, q.z, q.w};
+            asm volatile("" : "+v"(v));
+            uk[b0 + bb][s] = make_uint4(v.x, v.y, v.z, v.w);
+          }
+      }
 #pragma unroll
       for (int bb = 0; bb < RBB; bb++) {
         const int b = b0 + bb;
@@ -902,11 +965,16 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     else
       sweep2(std::false_type(), std::true_type());
   };
-  issue(0, bufA, rbA);
+  uint4 regA[RB][NSEG], regB[RB][NSEG];
+  float roldA = 0.f, roldB = 0.f;
+  if constexpr (REG)
+    issue_reg(0, regA, roldA);
+  else
+    issue(0, bufA, rbA);
   for (int64_t blk = 0; blk < nblk; blk += 2) {
-    step(blk, bufA, rbA, bufB, rbB);
+    step(blk, bufA, rbA, bufB, rbB, regA, roldA, regB, roldB);
     if (blk + 1 >= nblk) break;
-    step(blk + 1, bufB, rbB, bufA, rbA);
+    step(blk + 1, bufB, rbB, bufA, rbA, regB, roldB, regA, roldA);
   }
   __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);
   __syncthreads();

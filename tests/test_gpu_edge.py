@@ -139,6 +139,39 @@ def test_row_band_widths_with_partial_chunks(hp):
     assert st.compared > 0
 
 
+def test_row_strides_past_a_32_bit_block_span():
+    """Aligned expert rows whose stride makes one block of rows span 2^31 bytes or more: the
+    row-band pass addresses a block by 32-bit offsets in its aligned variant, so such a tensor
+    takes the element-load variant. Beside it, a large stride below that limit keeps the
+    aligned one. Both against the oracle (the last block of each band is partial), and the
+    memory between the rows stays untouched."""
+    dev = torch.device("cuda")
+    specs = [W.Spec("ex.far", W.EXPERT, (5, 8192), 0), W.Spec("ex.near", W.EXPERT, (6, 8192), 1)]
+    wl = W.Workload("row_strides", specs, 3)
+    strides = ((1 << 28) + 8, (1 << 20) + 8)
+    log("[parity] expert rows at strides 2^28 + 8 and 2^20 + 8, 3 steps")
+    bases, Ws, Gs = [], [], []
+    for s, ld in zip(specs, strides):
+        n, m = s.shape
+        wb = torch.zeros((n - 1) * ld + m, dtype=torch.bfloat16, device=dev)
+        gb = torch.zeros_like(wb)
+        w = wb.as_strided((n, m), (ld, 1))
+        w.copy_(W.init_weight(s, wl, dev))
+        bases.append((wb, gb))
+        Ws.append(w)
+        Gs.append(gb.as_strided((n, m), (ld, 1)))
+    pr = ParityRun(wl, weights=Ws, grads=Gs)
+    for t in range(1, 4):
+        pr.step(t)
+    assert pr.stats.ok(), pr.stats
+    assert pr.stats.compared == 3 * sum(s.numel for s in wl.specs)
+    for (wb, gb), w, g in zip(bases, Ws, Gs):
+        assert torch.count_nonzero(wb) == torch.count_nonzero(w)
+        assert torch.count_nonzero(gb) == torch.count_nonzero(g)
+    del bases, Ws, Gs, pr
+    torch.cuda.empty_cache()
+
+
 def test_overlapping_row_views_are_refused_before_any_launch():
     """A view whose rows overlap (an expanded row, or an unfold window: row stride below the
     row length) would make the in-place update write past the view; the binding refuses it

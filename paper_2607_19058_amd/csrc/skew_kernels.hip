@@ -1351,11 +1351,12 @@ __device__ __forceinline__ SumPair p2_factored(const DevTensor &t, const Tile &t
   SumPair acc = {0.0, 0.0};
   if (col >= m) return acc;
   float cp[8];    // c'_j = C_j / q, rounded as the oracle
-  double bd[8];   // 1/sqrt(c'_j)
+  double bd[8];   // 1/sqrt(c'_j) to about 2^-50 (it scales the unrounded estimate only)
 #pragma unroll
   for (int e = 0; e < 8; e++) {
     cp[e] = (col + e < m) ? ldg(t.C + col + e) / q : 0.f;
-    bd[e] = 1.0 / sqrt((double)cp[e]);
+    const double cd = (double)cp[e];
+    bd[e] = (cp[e] > 0.f && cp[e] < __builtin_inff()) ? rsq_d(cd) : 1.0 / sqrt(cd);
   }
   auto elem = [&](float x, float Ri, double ai, int e, SumPair &a) {
     const float ax = __fmul_rn(s, x);
@@ -1599,7 +1600,7 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
     const Tile tl = tile_of(t, tile / kSub);
     const int prt = tile % kSub;
     if (j != qj) {
-      q = mean_r_clamped(t, k, sh);
+      q = ldg(&t.sc->q);   // the clip stage's q (the one the update pass takes)
       qj = j;
     }
     if (level == 1) {

@@ -40,6 +40,8 @@ struct TensorScalars {
   int32_t ambiguous;  // bits 0..3: kClip* (how k was decided); bits 4..7: why a re-check ran (kWhy*)
   int32_t regime;     // row-band tensors, set by the clip stage for the next step: which sums the
                       // row-band pass forms (kRegime*); zero (both) after skew_state_init
+  float split_spread; // relative spread of the last floor-split re-check's sum (0: none yet)
+  int32_t pad;
 };
 // Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
 // launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for

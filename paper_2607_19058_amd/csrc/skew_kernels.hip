@@ -1685,6 +1685,7 @@ __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor 
   if (threadIdx.x == 0) {
     bool amb = false;
     const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
+    if (level == 1) stg(&t0.sc->split_spread, (float)spread);   // for the next step's routing
     kf_sh = clip_from_sum(S, N, k.d, spread, amb);
     amb_sh = amb;
     pos_sh = amb ? atomicAdd(&L->n2, ng) : 0;
@@ -1927,8 +1928,17 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
       if (!(sqrt(S / N) / (double)k.d < 1.0) && !amb) {
         amb = true;
         // the floor split per element decides most of these, except where the factors
-        // repeat (its spread is statistical too)
-        level = rep_any ? 2 : 1;
+        // repeat (its spread is statistical too). A tensor whose terms left the split's
+        // spread wide (heavy tails) keeps them from step to step: when the last split's
+        // relative spread makes an undecided k likely (more than 0.55 of the spacing of k's
+        // floats near the estimate: the exact sequence costs about 1/0.45 of the split's
+        // vector work), it goes straight to the exact sequence. Every eighth step takes
+        // the split, which renews the spread. The choice only saves a pass.
+        const double r = sqrt(S / N) / (double)k.d;
+        const float kg = (float)(1.0 / r);
+        const double gap = (double)nextafterf(kg, 3.0e38f) - (double)kg;
+        const bool wide = (double)ldg(&t0.sc->split_spread) * (1.0 / r) > 0.55 * gap && (k.step & 7) != 0;
+        level = (rep_any || wide) ? 2 : 1;
       }
     } else {
       spread = S > 0.0 ? err / S : 0.0;

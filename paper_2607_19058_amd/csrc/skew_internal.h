@@ -42,6 +42,7 @@ struct TensorScalars {
                       // row-band pass forms (kRegime*); zero (both) after skew_state_init
   float split_spread; // relative spread of the last floor-split re-check's sum (0: none yet)
   int32_t pad;
+  double s_fast, e_fast;  // the clip stage's fast sum of this slice and its error bound (stacks)
 };
 // Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
 // launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for

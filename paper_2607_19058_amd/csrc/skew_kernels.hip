@@ -1548,7 +1548,9 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const DevTensor *__re
   if (n <= 0) return;
   const int32_t *list = recheck_list(L, ntensors, level);
   auto tiles = [&](int j) {
-    const DevTensor &t = TT[ldg(list + j)];
+    const int32_t ti = ldg(list + j);
+    if (ti < 0) return (int64_t)0;   // a slice of a stack whose fast sum is kept
+    const DevTensor &t = TT[ti];
     return (int64_t)t.ntr * t.ntc * kSub;   // per-part sums
   };
   const bool table = n <= kTable;
@@ -1646,45 +1648,57 @@ __global__ __launch_bounds__(kThreads) void clip_recheck_kernel(const DevTensor 
                                                                 int ntensors, StepConsts k, int level) {
   __shared__ double sh[kThreads];
   __shared__ double wsum[kWaves][3];
+  __shared__ double wek[kWaves];
   __shared__ float kf_sh;
   __shared__ int amb_sh, pos_sh;
   const int n = ldg(level == 1 ? &L->n1 : &L->n2);
   if ((int)blockIdx.x >= n) return;
   const int ti = ldg(recheck_list(L, ntensors, level) + blockIdx.x);
+  if (ti < 0) return;
   const DevTensor &t0 = TT[ti];
   if (t0.grp0 != ti) return;
   const int ng = t0.ngrp;
-  double S = 0.0, Q4 = 0.0, N = 0.0;
+  double S = 0.0, Q4 = 0.0, N = 0.0, Ek = 0.0;   // Ek: error bounds of the kept fast sums
   if (ng == 1) {
     const int64_t ntiles = (int64_t)t0.ntr * t0.ntc * kSub;   // per-part sums
     S = red_sum(RedGroup{sh}, t0.ssum, ntiles);
     if (level == 1) Q4 = red_sum(RedGroup{sh}, t0.qsum, ntiles);
     N = (double)(t0.n * t0.m);
   } else {
+    // level 1 re-read only the stack's open slices (and its first); the others, listed as
+    // -1 (the group's entries are consecutive from this one), keep the clip stage's fast
+    // sum and its error bound
     const int w = (int)(threadIdx.x >> 6);
-    double s = 0.0, q4 = 0.0, nn = 0.0;
+    double s = 0.0, q4 = 0.0, nn = 0.0, ek = 0.0;
     for (int e = w; e < ng; e += kWaves) {
       const DevTensor &t = TT[ti + e];
       const int64_t ntiles = (int64_t)t.ntr * t.ntc * kSub;
-      s += red_sum(RedWave{}, t.ssum, ntiles);
-      if (level == 1) q4 += red_sum(RedWave{}, t.qsum, ntiles);
+      if (level == 1 && ldg(recheck_list(L, ntensors, 1) + blockIdx.x + e) < 0) {
+        s += ldg(&t.sc->s_fast);
+        ek += ldg(&t.sc->e_fast);
+      } else {
+        s += red_sum(RedWave{}, t.ssum, ntiles);
+        if (level == 1) q4 += red_sum(RedWave{}, t.qsum, ntiles);
+      }
       nn += (double)(t.n * t.m);
     }
     if ((threadIdx.x & 63) == 0) {
       wsum[w][0] = s;
       wsum[w][1] = q4;
       wsum[w][2] = nn;
+      wek[w] = ek;
     }
     __syncthreads();
     for (int v = 0; v < kWaves; v++) {   // waves in order
       S += wsum[v][0];
       Q4 += wsum[v][1];
       N += wsum[v][2];
+      Ek += wek[v];
     }
   }
   if (threadIdx.x == 0) {
     bool amb = false;
-    const double spread = level == 1 ? 20.0 * 0x1p-23 * sqrt(Q4) / S + 1e-14 : 0.0;
+    const double spread = level == 1 ? (20.0 * 0x1p-23 * sqrt(Q4) + Ek) / S + 1e-14 : 0.0;
     if (level == 1) stg(&t0.sc->split_spread, (float)spread);   // for the next step's routing
     kf_sh = clip_from_sum(S, N, k.d, spread, amb);
     amb_sh = amb;
@@ -1859,6 +1873,10 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   __shared__ int wflag[kWaves][4];
   __shared__ float kf_sh;
   __shared__ int st_sh, pos_sh;
+  // a stack's open slices, for a floor-split re-check of those alone (stacks of up to
+  // kOpenBits slices; a larger one re-reads every slice)
+  constexpr int kOpenBits = 32 * 64;
+  __shared__ uint32_t openbits[kOpenBits / 32];
   const Item it = items[blockIdx.x];   // the first sub-tensor of a group sharing one k
   const DevTensor &t0 = TT[it.tensor];
   const int g0 = t0.grp0, ng = t0.ngrp;
@@ -1876,12 +1894,20 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     bad_any = o.bad != 0;
     rep_any = o.repeats != 0;
   } else {
+    for (int q = (int)threadIdx.x; q < kOpenBits / 32; q += kThreads) openbits[q] = 0u;
+    __syncthreads();
     const int w = (int)(threadIdx.x >> 6);
     double s = 0.0, e_ = 0.0, nn = 0.0;
     int first = 0x7fffffff, why = 0, bad = 0, rep = 0;   // the wave's first open slice, and why it is open
     for (int e = w; e < ng; e += kWaves) {
       const DevTensor &t = TT[g0 + e];
       const SliceSum o = slice_sum(t, k, RedWave{});
+      if ((threadIdx.x & 63) == 0) {
+        // kept for the re-check, should the stack's sum be open
+        stg(&t.sc->s_fast, o.S);
+        stg(&t.sc->e_fast, o.E);
+        if (o.open && e < kOpenBits) atomicOr(&openbits[e >> 5], 1u << (e & 31));
+      }
       s += o.S;
       e_ += o.E;
       nn += (double)(t.n * t.m);
@@ -1953,11 +1979,15 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
   __syncthreads();
   const float kf = kf_sh;
   const int st = st_sh, pos = pos_sh;
+  // a stack's floor-split re-check reads its first slice (whose work-group decides k) and
+  // its open slices; the others are listed as -1 and keep their fast sums
+  const bool partial = (st >> 16) == 1 && ng > 1 && ng <= kOpenBits;
   for (int e = (int)threadIdx.x; e < ng; e += kThreads) {
     const DevTensor &t = TT[g0 + e];
     stg(&t.sc->k, kf);
     if (st >= 0) {
-      stg(recheck_list(L, ntensors, st >> 16) + pos + e, (int32_t)(g0 + e));
+      const bool keep = partial && e > 0 && !((openbits[e >> 5] >> (e & 31)) & 1u);
+      stg(recheck_list(L, ntensors, st >> 16) + pos + e, keep ? (int32_t)-1 : (int32_t)(g0 + e));
       stg(&t.sc->ambiguous, (int32_t)(st & 0xFFFF));
     } else {
       stg(&t.sc->ambiguous, (int32_t)kClipFast);

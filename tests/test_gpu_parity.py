@@ -133,6 +133,31 @@ def test_layer_every_tensor():
 
 
 @pytest.mark.timeout(900)
+def test_layer_stacked_every_tensor_and_partial_split():
+    """The layer with each expert projection stacked into one (128, n, m) tensor that shares
+    one clip factor: when a stack's sum is open, the floor-split re-check re-reads only its
+    open slices (and its first) and keeps the others' fast sums. Every tensor compared at
+    step 2 and, until a stack has taken that re-check on a compared step, at later ones."""
+    wl = W.stacked(W.get("layer"))
+    log("[parity] layer with stacked experts: every tensor compared, a stack decided by the floor split")
+    sp = StreamParity(wl)
+    stacks = [k for k, s in enumerate(wl.specs) if len(s.shape) == 3]
+    assert stacks
+    split_seen = False
+    for t in range(1, 6):
+        routes = sp.step(t, snapshot=t >= 2)
+        if t >= 2:
+            st = sp.compare_last()
+            assert st.ok(), (t, st)
+            log(f"    routes at step {t}: {_route_log(routes, wl.specs)}; stacks {[routes[k] for k in stacks]}")
+            split_seen |= any(routes[k] == 4 for k in stacks)
+            if split_seen:
+                break
+    assert sp.stats.ok(), sp.stats
+    assert split_seen, "no stack took the floor-split re-check on a compared step"
+
+
+@pytest.mark.timeout(900)
 def test_stress_every_tensor_and_clip_routes():
     """Heavy-tailed stress (Student-t(2), 0.1% outliers x100, 90% sparse experts): every
     tensor at each of its 5 steps, and each way of deciding the clip factor taken by at least

@@ -32,7 +32,7 @@ struct skew_ctx {
   char *ws = nullptr;   // workspace base (device)
   DevTensor *d_table = nullptr;
   RecheckLists *lists = nullptr;
-  ItemList p1, fold, p2, p3, clip, fold_rows;
+  ItemList p1, fold, p2, p3, clip, clip_slices, fold_rows;
   float *gscale = nullptr;   // device: the gradient-norm mode's scale
   double *gsq = nullptr;     // device: per-tensor sums of g^2
   ItemList z[kZVariants];    // row-band pass items, one list per kernel variant
@@ -233,7 +233,7 @@ int init_ctx(skew_ctx **ctx, Plan &p, skew_tensor_desc *d, int n, void *state, s
   Item *const base = reinterpret_cast<Item *>(ws + p.off_items);
   std::vector<Item> items;
   items.reserve(p.p1.size() + p.z.size() + p.fold.size() + p.p2.size() + p.p3.size() + p.clip.size() +
-                p.fold_rows.size() + 1);
+                p.clip_slices.size() + p.fold_rows.size() + 1);
   auto add = [&](ItemList &l, const std::vector<Item> &v) {
     l.d = base + items.size();
     l.n = (int64_t)v.size();
@@ -245,6 +245,7 @@ int init_ctx(skew_ctx **ctx, Plan &p, skew_tensor_desc *d, int n, void *state, s
   add(c->p2, p.p2);
   add(c->p3, p.p3);
   add(c->clip, p.clip);
+  add(c->clip_slices, p.clip_slices);
   add(c->fold_rows, p.fold_rows);
   if (items.empty()) items.push_back({0, 0});
   if (sizeof(Item) * items.size() > p.off_lists - p.off_items) {   // the planner's region must hold them
@@ -370,6 +371,8 @@ int skew_step(skew_ctx *ctx, const skew_hparams *hp, void *stream) {
   // empty lists exit at once), then the update
   if (ctx->p2.n > 0) run(4, [&] { return launch_p2(T, ctx->p2.d, ctx->p2.n, k, s); });
   if (ctx->clip.n > 0) {
+    if (ctx->clip_slices.n > 0)
+      run(5, [&] { return launch_clip_slices(T, ctx->clip_slices.d, ctx->clip_slices.n, k, s); });
     run(5, [&] { return launch_clip(T, ctx->clip.d, ctx->clip.n, k, L, nt, s); });
     run(6, [&] { return launch_recheck(T, L, nt, k, 1, s); });
     run(7, [&] { return launch_clip_recheck(T, L, nt, k, 1, s); });

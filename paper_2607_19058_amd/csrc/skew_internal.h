@@ -41,8 +41,9 @@ struct TensorScalars {
   int32_t regime;     // row-band tensors, set by the clip stage for the next step: which sums the
                       // row-band pass forms (kRegime*); zero (both) after skew_state_init
   float split_spread; // relative spread of the last floor-split re-check's sum (0: none yet)
-  int32_t pad;
-  double s_fast, e_fast;  // the clip stage's fast sum of this slice and its error bound (stacks)
+  int32_t fast_flags; // stacks: the slice's fast sum is open (bits 0..3: why), non-finite
+                      // (bit 4), has repeated factors (bit 5)
+  double s_fast, e_fast;  // stacks: the slice's fast sum and its error bound
 };
 // Tensors the clip stage sends to a re-check, listed on the device (so that a re-check
 // launch covers only their tiles): l1 for the re-check with the exact floor split, l2 for
@@ -190,6 +191,7 @@ struct Plan {
   size_t off_gscale = 0;                      // workspace offset of the gradient scale (float)
   size_t off_gsq = 0;                         // workspace offset of the per-tensor sums of g^2
   std::vector<Item> p1, fold, p2, p3, clip;   // clip: one item per non-empty tensor
+  std::vector<Item> clip_slices;              // every slice of the stacked tensors
   // fold items of the gradient-norm mode's first fold: rows and columns of every factored
   // tensor (row-band tensors: rows [0, ceil(n / kFold)), then columns)
   std::vector<Item> fold_rows;
@@ -228,6 +230,8 @@ int launch_gnorm(const DevTensor *T, int ntensors, const StepConsts &k, void *st
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
               void *stream);
+// the clip stage's fast sum of every slice of the stacked tensors (one wave per slice)
+int launch_clip_slices(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream);
 int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,
                 int ntensors, void *stream);
 // re-check of the listed tensors: level 1 (exact floor split) or 2 (exact float sequence),

@@ -1856,6 +1856,23 @@ __device__ __forceinline__ SliceSum slice_sum(const DevTensor &t, const StepCons
   return o;
 }
 
+// The clip stage's share of each slice of the stacked tensors, one wave per slice: its fast
+// sum, error bound and flags (kept in its scalars for the group's decision and, should the
+// stack's sum be open, for its re-check), its q and its next regime.
+__global__ __launch_bounds__(kThreads) void clip_slices_kernel(const DevTensor *__restrict__ TT,
+                                                               const Item *__restrict__ items, int64_t count,
+                                                               StepConsts k) {
+  const int64_t j = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (j >= count) return;   // a whole wave
+  const DevTensor &t = TT[items[j].tensor];
+  const SliceSum o = slice_sum(t, k, RedWave{});
+  if ((threadIdx.x & 63) == 0) {
+    stg(&t.sc->s_fast, o.S);
+    stg(&t.sc->e_fast, o.E);
+    stg(&t.sc->fast_flags, (int32_t)((o.open & 15) | (o.bad ? 16 : 0) | (o.repeats ? 32 : 0)));
+  }
+}
+
 // --------------------------------------------------------------------------------------------
 // clip stage, one work-group per tensor (or per stacked tensor, whose slices share one k):
 // k = 1 / max(1, RMS(U_hat) / d) (Sec. 3, Alg. 1), NaN-propagating and rounded once to
@@ -1894,6 +1911,7 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     bad_any = o.bad != 0;
     rep_any = o.repeats != 0;
   } else {
+    // the slices' sums come from clip_slices_kernel (launched just before)
     for (int q = (int)threadIdx.x; q < kOpenBits / 32; q += kThreads) openbits[q] = 0u;
     __syncthreads();
     const int w = (int)(threadIdx.x >> 6);
@@ -1901,13 +1919,9 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(const DevTensor *__restr
     int first = 0x7fffffff, why = 0, bad = 0, rep = 0;   // the wave's first open slice, and why it is open
     for (int e = w; e < ng; e += kWaves) {
       const DevTensor &t = TT[g0 + e];
-      const SliceSum o = slice_sum(t, k, RedWave{});
-      if ((threadIdx.x & 63) == 0) {
-        // kept for the re-check, should the stack's sum be open
-        stg(&t.sc->s_fast, o.S);
-        stg(&t.sc->e_fast, o.E);
-        if (o.open && e < kOpenBits) atomicOr(&openbits[e >> 5], 1u << (e & 31));
-      }
+      const int fl = ldg(&t.sc->fast_flags);
+      const SliceSum o = {ldg(&t.sc->s_fast), ldg(&t.sc->e_fast), fl & 15, (fl >> 4) & 1, (fl >> 5) & 1};
+      if ((threadIdx.x & 63) == 0 && o.open && e < kOpenBits) atomicOr(&openbits[e >> 5], 1u << (e & 31));
       s += o.S;
       e_ += o.E;
       nn += (double)(t.n * t.m);
@@ -2301,6 +2315,13 @@ int launch_gnorm(const DevTensor *T, int ntensors, const StepConsts &k, void *st
 int launch_p2(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(p2_kernel, dim3((uint32_t)count), dim3(kThreads), 0, (hipStream_t)stream, T, items, k);
+  return (int)hipGetLastError();
+}
+int launch_clip_slices(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, void *stream) {
+  if (count <= 0) return hipSuccess;
+  const int64_t groups = (count + kWaves - 1) / kWaves;
+  hipLaunchKernelGGL(clip_slices_kernel, dim3((uint32_t)groups), dim3(kThreads), 0, (hipStream_t)stream, T, items,
+                     count, k);
   return (int)hipGetLastError();
 }
 int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &k, RecheckLists *L,

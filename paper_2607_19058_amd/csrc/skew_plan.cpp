@@ -163,6 +163,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
     tp.off_qsum = ws_part; ws_part = align_up(ws_part + (size_t)tiles * kSub * 8);
     tp.off_sc = ws_part; ws_part = align_up(ws_part + sizeof(TensorScalars));
     if (e == 0) p.clip.push_back({i, 0});   // one clip item per group (its first slice)
+    if (E > 1) p.clip_slices.push_back({i, 0});
     // the row-band pass (see rowband_shape)
     const RowBandShape rbs = rowband_shape(tp.m, tp.momentum != 0);
     const int64_t zcw = rbs.zcw, nseg = rbs.nseg, rpi = rbs.rpi, zrb = rbs.zrb;
@@ -240,7 +241,7 @@ int plan_build(const skew_tensor_desc *d, int n, Plan *out) {
   // and split into row-band and other tensors)
   p.off_items = ws;
   ws = align_up(ws + sizeof(Item) * (p.p1.size() + p.z.size() + 2 * p.fold.size() + p.p2.size() + p.p3.size() +
-                                     p.clip.size() + p.fold_rows.size() + 1));
+                                     p.clip.size() + p.clip_slices.size() + p.fold_rows.size() + 1));
   p.off_lists = ws;
   ws = align_up(ws + sizeof(RecheckLists) + sizeof(int32_t) * 2 * (size_t)std::max(nt, 1));
   p.off_zero = ws;   // zero-filled with the workspace at set-up and never written

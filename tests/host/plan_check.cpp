@@ -108,7 +108,11 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
   for (int64_t q = 0; q < count; q++) {
     const DevTensor &t = T[items[q].tensor];
     const int lg = t.nseg == 1 ? 0 : (t.nseg == 2 ? 1 : (t.nseg == 4 ? 2 : 3));
-    CHECK(variant == lg * 4 + (t.vec ? 0 : 2) + (t.momentum ? 1 : 0), "row-band variant %d", variant);
+    // the aligned variants without momentum and up to two chunks per wave address a block by
+    // 32-bit offsets: a wider block span takes the element-load variant
+    const bool wide_span = (int64_t)t.zrpi * t.zrb * t.ld * 2 > 0x7FFFFFFF;
+    const bool vec = t.vec && !(wide_span && !t.momentum && t.nseg <= 2);
+    CHECK(variant == lg * 4 + (vec ? 0 : 2) + (t.momentum ? 1 : 0), "row-band variant %d", variant);
   }
   return 0;
 }
@@ -131,6 +135,10 @@ int launch_p3(const DevTensor *T, const Item *items, int64_t count, const StepCo
 }
 int launch_clip(const DevTensor *T, const Item *items, int64_t count, const StepConsts &, RecheckLists *, int, void *) {
   check_items("clip", T, items, count);
+  return 0;
+}
+int launch_clip_slices(const DevTensor *T, const Item *items, int64_t count, const StepConsts &, void *) {
+  check_items("clip_slices", T, items, count);
   return 0;
 }
 int launch_recheck(const DevTensor *, RecheckLists *, int, const StepConsts &, int, void *) { return 0; }
@@ -336,6 +344,16 @@ static void check_init_and_step(const std::string &name, std::vector<skew_tensor
   };
   same("p3", p.p3);
   same("clip", p.clip);
+  same("clip_slices", p.clip_slices);
+  {
+    // the clip stage's slice items: every non-empty slice of a stacked tensor, once
+    std::multiset<std::pair<int, int>> want;
+    for (int i = 0; i < g_buf.nt; i++)
+      if (!p.t[i].empty && p.t[i].ngrp > 1) want.insert({i, 0});
+    std::multiset<std::pair<int, int>> got;
+    for (const Item &it : p.clip_slices) got.insert({it.tensor, it.tile});
+    CHECK(got == want, "%s: clip slice items %zu, stacked slices %zu", name.c_str(), got.size(), want.size());
+  }
   same("p1", p.p1);
   same(gnorm ? "z1" : "z0", p.z);
   if (gnorm) {

@@ -10,7 +10,9 @@
 //   p2    exact-second-moment tensors and wide factored ones: per tile, sum of squares of
 //         the unclipped update (Alg. 1)
 //   clip  per tensor: the clip factor k, and whether its rounding needs the exact pass
-//   p2x   exact re-run of the sum for the tensors the clip stage left undecided; clip again
+//         (the slices of stacked tensors first, one wave each, in a launch of their own)
+//   p2x   re-runs of the sum for the tensors the clip stage left undecided (the exact floor
+//         split, then the oracle's float sequence); clip again
 //   p3    every tensor: momentum / exact-v update, weight update, dithered bf16
 //         write-back (Sec. 3 "Update clipping and low-precision updates")
 // Reductions are deterministic (fixed-order partials; no float atomics), so two
@@ -395,10 +397,13 @@ __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restric
 // square root and the quotient; the per-band maximum of (s x)^2 / R_i bounds their spread.
 //
 // Staging: blocks of zrpi * zrb whole rows (bf16 gradient, and fp32 momentum on the
-// backbone) move into one of two LDS buffers while the other is being summed: with the
-// direct global-to-LDS loads (16 bytes per lane) when rows are 16-byte aligned, through
-// registers otherwise. No register holds data in flight, so a 512-thread work-group with
-// up to 256 VGPRs per wave keeps a whole block (up to 64 KiB) of loads outstanding.
+// backbone). Aligned rows without momentum and with one or two chunks per wave (the normal
+// step) stage in registers: each wave loads its own pieces of the next block by buffer
+// loads while it sums the current one. The other variants move a block into one of two LDS
+// buffers while the other is being summed: with the direct global-to-LDS loads (16 bytes
+// per lane) when rows are 16-byte aligned, through registers otherwise; no register holds
+// their data in flight, so a 512-thread work-group with up to 256 VGPRs per wave keeps a
+// whole block (up to 64 KiB) of loads outstanding.
 //
 // Layout: zcw 512-column chunks per row; a group of wpr = ceil(zcw / NSEG) waves shares a
 // row, wave w of the group taking chunks w, w + wpr, ...; zrpi = 8 / wpr groups work on

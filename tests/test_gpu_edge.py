@@ -245,3 +245,55 @@ def test_structured_gradients_clip_factor_matches_the_oracle():
             routes_seen.add(route[k] & 0xF)
     log(f"  total: {pr.stats}; clip routes seen {sorted(routes_seen)}")
     assert pr.stats.ok(), pr.stats
+
+
+def test_two_contexts_on_two_streams_match_serial_runs():
+    """Two contexts stepped at the same time on two streams, each with its own state and
+    workspace, end with the weights, state and clip factors, bit for bit, of the same two
+    contexts stepped one after the other on one stream: no device memory is shared between
+    contexts. One context takes the gradient-norm scaling and the decay, the other the plain
+    step; the second holds row-band, wide (pass 1 by tiles), stacked, vector and router
+    tensors large enough for the two steps' kernels to overlap."""
+    dev = torch.device("cuda", 0)
+    shapes_b = [("ex.a", W.EXPERT, (1024, 4096)), ("ex.b", W.EXPERT, (4096, 1024)),
+                ("ex.stack", W.EXPERT, (2, 512, 2048)), ("bb", W.BACKBONE, (1024, 2048)),
+                ("bb.wide", W.BACKBONE, (64, 20000)), ("bb.vec", W.BACKBONE, (2048,)), ("rt", W.ROUTER, (2048, 64))]
+    wl_b = W.Workload("two_streams", [W.Spec(n, tier, shape, k) for k, (n, tier, shape) in enumerate(shapes_b)], 3)
+    hps = [dict(weight_decay=0.05, max_grad_norm=1e-2), dict()]
+    runs = []   # per workload: gradients, weights of the concurrent and of the serial run, contexts
+    for wl in (W.get("tiny"), wl_b):
+        G = [torch.empty(s.shape, dtype=torch.bfloat16, device=dev) for s in wl.specs]
+        Wc = [W.init_weight(s, wl, dev) for s in wl.specs]
+        Ws = [w.clone() for w in Wc]
+
+        def make(Wt, wl=wl, G=G):
+            return SkewAdam([(s.tier, Wt[k], G[k], s.tensor_id, s.state_flags) for k, s in enumerate(wl.specs)])
+        runs.append((wl, G, Wc, Ws, make(Wc), make(Ws)))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    main = torch.cuda.current_stream()
+    for t in (1, 2, 3):
+        for wl, G, *_ in runs:
+            sc = W.expert_scales(wl, t)
+            for k, s in enumerate(wl.specs):
+                W.fill_grad(s, wl, t, G[k], sc)
+        torch.cuda.synchronize()
+        ready = torch.cuda.Event()
+        ready.record(main)
+        for j, run_j in enumerate(runs):
+            streams[j].wait_event(ready)
+            run_j[4].step(t, stream=streams[j], **hps[j])
+        torch.cuda.synchronize()
+        for j, run_j in enumerate(runs):
+            run_j[5].step(t, stream=main, **hps[j])
+        torch.cuda.synchronize()
+    for wl, G, Wc, Ws, oc, osr in runs:
+        log(f"two streams: {wl.name}, {len(wl.specs)} tensors compared bit for bit")
+        for k, s in enumerate(wl.specs):
+            assert torch.equal(Wc[k].view(torch.uint8), Ws[k].view(torch.uint8)), (wl.name, s.name, "w")
+            vc, vs = oc.state_views(k), osr.state_views(k)
+            assert vc.keys() == vs.keys()
+            for name in vc:
+                assert torch.equal(vc[name].view(torch.uint8), vs[name].view(torch.uint8)), (wl.name, s.name, name)
+        assert oc.clip_info() == osr.clip_info()
+        oc.close()
+        osr.close()

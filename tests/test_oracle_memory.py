@@ -68,7 +68,7 @@ def test_parameter_counts():
     _check("params_norms", _count(oracle.BACKBONE, ndim=1))
     _check("params_total", _count())
     _check("weights_bf16_gib", 2 * _count())
-    # exact tier sizes that the survey of App. B derives
+    # exact tier sizes of the App. B architecture (its layer inventory counted out)
     assert _count(oracle.BACKBONE) == 341_352_448
     assert _count(oracle.EXPERT) == 6_442_450_944
     assert _count(oracle.ROUTER) == 524_288

@@ -158,14 +158,15 @@ __device__ __forceinline__ float dither_hi(uint32_t h) { return dither_u16(h >> 
 __device__ __forceinline__ float dither_of(uint32_t h, uint64_t idx) { return (idx & 1u) ? dither_hi(h) : dither_lo(h); }
 
 // The noise added before the cast is the product of two exact factors: e 2^-24 and |w|
-// (ulp(w) taken as 2^-7 |w|, Sec. 3), or, in the exact-ulp mode, e 2^-17 and the bf16 ulp
-// of w: 2^(E - 134) for biased exponent E >= 1, 2^-133 among the subnormals
-__device__ __forceinline__ float bf16_ulp(float w) {
-  const uint32_t E = (__float_as_uint(w) >> 23) & 0xFFu;
-  return __uint_as_float(E >= 8u ? (E - 7u) << 23 : 1u << ((E > 0u ? E : 1u) + 15u));
+// (ulp(w) taken as 2^-7 |w|, Sec. 3), or, in the exact-ulp mode, e 2^-24 and 2^7 times the
+// bf16 ulp of w. That ulp is 2^(E - 134) for biased exponent E >= 1 and 2^-133 among the
+// subnormals, so 2^7 ulp is the float whose exponent field is E clamped to [1, 254] (an
+// infinite or NaN w keeps a finite factor; its update is infinite or NaN already)
+__device__ __forceinline__ float bf16_ulp128(float w) {
+  const uint32_t b = __float_as_uint(w) & 0x7F800000u;
+  return __uint_as_float(min(max(b, 0x00800000u), 0x7F000000u));
 }
-__device__ __forceinline__ float dither_mul(float w, bool xu) { return xu ? bf16_ulp(w) : fabsf(w); }
-__device__ __forceinline__ float dither_fac(float dith, bool xu) { return xu ? dith * 128.f : dith; }
+__device__ __forceinline__ float dither_mul(float w, bool xu) { return xu ? bf16_ulp128(w) : fabsf(w); }
 
 // fixed-order tree over the work-group (every thread gets the total)
 __device__ __forceinline__ double block_sum(double x, double *sh) {
@@ -2028,7 +2029,7 @@ __device__ __forceinline__ float exact_factored_y(float x, float w, float wd, fl
   const float vh = __fmul_rn(Ri, cpj);
   const float dd = sqrtf(max_nan(vh, eps));
   const float U = __fmul_rn(__fmul_rn(s, x) / dd, kc);
-  return fmaf(dither_fac(dith, xu), dither_mul(w, xu), fmaf(-lr, U, wd));
+  return fmaf(dith, dither_mul(w, xu), fmaf(-lr, U, wd));
 }
 
 // y may round differently from the oracle's value when this is >= 0: the fast update x*F
@@ -2087,7 +2088,7 @@ __device__ __forceinline__ void p3_row8(const DevTensor &t, const StepConsts &k,
 #pragma unroll
   for (int e = 0; e < 8; e++) {
     const float F = fminf(alpha * bf[e], c.cap3);
-    y[e] = fmaf(dither_fac(dith[e], xu), dither_mul(w[e], xu), fmaf(-x[e], F, decayed(w[e], dec, k.wd)));
+    y[e] = fmaf(dith[e], dither_mul(w[e], xu), fmaf(-x[e], F, decayed(w[e], dec, k.wd)));
     slack = fmaxf(slack, boundary_slack(y[e], x[e] * F, w[e]));
   }
   if (slack >= 0.f) {
@@ -2160,7 +2161,7 @@ __device__ __forceinline__ void p3_factored(const DevTensor &t, const Tile &tl, 
         const float F = fminf(alpha * (float)col_factor(t, col + e, c.q), c.cap3);
         const float wd = decayed(w, DEC && t.decay, k.wd);
         constexpr bool xu = XU;
-        float y = fmaf(dither_fac(dith, xu), dither_mul(w, xu), fmaf(-x, F, wd));
+        float y = fmaf(dith, dither_mul(w, xu), fmaf(-x, F, wd));
         if (near_boundary(y, x * F, w))
           y = exact_factored_y(x, w, wd, ldg(t.R + i), ldg(t.C + col + e) / c.q, c.s, kc, k.eps, k.lr, dith, xu);
         stg(t.w + i * ld + col + e, to_bf16(y));
@@ -2205,7 +2206,7 @@ __device__ __forceinline__ void p3_exact(const DevTensor &t, const Tile &tl, con
       }
       const uint64_t idx = (uint64_t)(t.idx0 + sidx);
       constexpr bool xu = XU;
-      const float y = fmaf(dither_fac(dither_of(dz.pair(idx >> 1), idx), xu), dither_mul(w, xu), x);
+      const float y = fmaf(dither_of(dz.pair(idx >> 1), idx), dither_mul(w, xu), x);
       stg(t.w + i * ld + col + e, to_bf16(y));
     }
   }

@@ -778,7 +778,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     }
   };
   auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt,
-                  uint4 (&regc)[RB][NSEG], float rold, uint4 (&regn)[RB][NSEG], float &rnold) {
+                  uint4 (&regc)[RB][NSEG], float rold, uint4 (&regn)[RB][NSEG], float &rnold, auto zc, auto yc) {
     if constexpr (REG) {
       // the next block's loads go out first; the compiler waits for this block's registers
       // where they are first used
@@ -962,14 +962,8 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       }
       __builtin_amdgcn_sched_barrier(0);
     };
-    if (!active || mode == 1)
-      ;   // an idle wave (its rows are group 0's) adds nothing; mode 1 forms no update sums
-    else if (want_z && want_y)
-      sweep2(std::true_type(), std::true_type());
-    else if (want_z)
-      sweep2(std::true_type(), std::false_type());
-    else
-      sweep2(std::false_type(), std::true_type());
+    // an idle wave (its rows are group 0's) adds nothing; mode 1 forms no update sums
+    if (active && mode != 1) sweep2(zc, yc);
   };
   uint4 regA[RB][NSEG], regB[RB][NSEG];
   float roldA = 0.f, roldB = 0.f;
@@ -977,11 +971,20 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     issue_reg(0, regA, roldA);
   else
     issue(0, bufA, rbA);
-  for (int64_t blk = 0; blk < nblk; blk += 2) {
-    step(blk, bufA, rbA, bufB, rbB, regA, roldA, regB, roldB);
-    if (blk + 1 >= nblk) break;
-    step(blk + 1, bufB, rbB, bufA, rbA, regB, roldB, regA, roldA);
-  }
+  // the band's loop, specialised for the sums it forms (the regime is the same for the band)
+  auto band_loop = [&](auto zc, auto yc) {
+    for (int64_t blk = 0; blk < nblk; blk += 2) {
+      step(blk, bufA, rbA, bufB, rbB, regA, roldA, regB, roldB, zc, yc);
+      if (blk + 1 >= nblk) break;
+      step(blk + 1, bufB, rbB, bufA, rbA, regB, roldB, regA, roldA, zc, yc);
+    }
+  };
+  if (want_z && want_y)
+    band_loop(std::true_type(), std::true_type());
+  else if (want_z)
+    band_loop(std::true_type(), std::false_type());
+  else
+    band_loop(std::false_type(), std::true_type());
   __builtin_amdgcn_s_waitcnt(kWaitVmLgkm0);
   __syncthreads();
   // column partials: groups 1.. add theirs into group 0's through LDS, in group order

@@ -728,7 +728,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       for (int s = 0; s < NSEG; s++)
         vo[b][s] = sok[s] ? (uint32_t)((((int64_t)grp_c * RB + b) * ld + col[s]) * 2) : 0x80000000u;
   }
-  auto issue_reg = [&](int64_t blk, uint4 (&dst)[RB][NSEG], float &rold) {
+  auto issue_reg = [&](int64_t blk, u32x4_t (&dst)[RB][NSEG], float &rold) {
     const int64_t rbase = r0 + blk * br;
     const int64_t span = (r1 - rbase) * ld * 2;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -737,8 +737,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     for (int b = 0; b < RB; b++)
 #pragma unroll
       for (int s = 0; s < NSEG; s++) {
-        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[b][s], 0, 0);
-        dst[b][s] = make_uint4(v.x, v.y, v.z, v.w);
+        dst[b][s] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[b][s], 0, 0);
       }
     const int64_t i = rbase + rfold;
     rold = ldg(t.R + (i < r1 ? i : r1 - 1));
@@ -778,7 +777,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     }
   };
   auto step = [&](int64_t blk, unsigned char *cur, float *rcur, unsigned char *nxt, float *rnxt,
-                  uint4 (&regc)[RB][NSEG], float rold, uint4 (&regn)[RB][NSEG], float &rnold, auto zc, auto yc) {
+                  u32x4_t (&regc)[RB][NSEG], float rold, u32x4_t (&regn)[RB][NSEG], float &rnold, auto zc, auto yc) {
     if constexpr (REG) {
       // the next block's loads go out first; the compiler waits for this block's registers
       // where they are first used
@@ -802,7 +801,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 #pragma unroll
           for (int bb = 0; bb < RBB; bb++)
 #pragma unroll
-            for (int s = 0; s < NSEG; s++) uk[b0 + bb][s] = regc[b0 + bb][s];
+            for (int s = 0; s < NSEG; s++) uk[b0 + bb][s] = to_uint4(regc[b0 + bb][s]);
         } else {
           read_rows(cur, b0, uk);
         }
@@ -893,17 +892,15 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       if constexpr (!REG) {
         if (!KEEP || mode == 2) read_rows(cur, b0, uk);   // (mode 2: the first sweep did not run)
       } else {
-        // the packed block is unpacked again here (in place: the registers are not needed
-        // after this sweep); keeping sweep 1's floats beside the next block's registers would
-        // spill
+        // the packed block is unpacked again here, from its own registers (not needed after
+        // this sweep, so the empty asm may claim to change them: no copy is made); keeping
+        // sweep 1's floats beside the next block's registers would spill
 #pragma unroll
         for (int bb = 0; bb < RBB; bb++)
 #pragma unroll
           for (int s = 0; s < NSEG; s++) {
-            const uint4 &q = regc[b0 + bb][s];
-            u32x4_t v = {q.x, q.y, q.z, q.w};
-            asm volatile("" : "+v"(v));
-            uk[b0 + bb][s] = make_uint4(v.x, v.y, v.z, v.w);
+            asm volatile("" : "+v"(regc[b0 + bb][s]));
+            uk[b0 + bb][s] = to_uint4(regc[b0 + bb][s]);
           }
       }
 #pragma unroll
@@ -965,7 +962,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
     // an idle wave (its rows are group 0's) adds nothing; mode 1 forms no update sums
     if (active && mode != 1) sweep2(zc, yc);
   };
-  uint4 regA[RB][NSEG], regB[RB][NSEG];
+  u32x4_t regA[RB][NSEG], regB[RB][NSEG];
   float roldA = 0.f, roldB = 0.f;
   if constexpr (REG)
     issue_reg(0, regA, roldA);

@@ -850,7 +850,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       const float R = rcur[r];
       const double Rd = (double)R;
       const bool normal = R > 0.f && R < __builtin_inff();
-      winv_l = (R > 0.f && i < r1) ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
+      winv_l = (normal && i < r1) ? rcp_d(Rd) : 0.0;   // (1/R is 0 for R = +inf)
       if (active && wg == 0 && b < rb && w == 0 && i < r1) {
         rstash[i - r0] = R;
         if (R != R) bad_l = 1;
@@ -875,7 +875,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       const float R = fmaf(k.a2, ri, __fmul_rn(k.b2, Rold));
       const double Rd = (double)R;
       const bool normal = R > 0.f && R < __builtin_inff();
-      winv_l = (R > 0.f && i < r1) ? (normal ? rcp_d(Rd) : 1.0 / Rd) : 0.0;
+      winv_l = (normal && i < r1) ? rcp_d(Rd) : 0.0;   // (1/R is 0 for R = +inf)
       if (active && wg == 0 && b < rb && w == 0 && i < r1) {
         // staged for the band's end: a global store here would hold up the next block's
         // wait for its staged rows until the store completes

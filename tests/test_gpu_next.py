@@ -234,6 +234,32 @@ def test_exact_ulp_dither_unit_shapes_with_decay():
     assert st.ok(), st
 
 
+@pytest.mark.parametrize("flags,decay", [(0, 0.0), (2, 0.0), (2, 0.05)], ids=["plain", "exact_ulp", "exact_ulp+decay"])
+def test_weights_of_every_finite_bf16_value(flags, decay):
+    """Weights that take every finite bf16 value (both signs, every mantissa, biased exponents
+    0 to 254: zero, the subnormals and the largest binade) in a factored expert matrix, a
+    factored backbone matrix with momentum, an exact-V backbone vector and an exact-V router
+    matrix, 3 steps, every element against the oracle. The dither's width comes from |w| or,
+    in the exact-ulp mode, from w's exponent (clamped to the smallest normal binade for zero
+    and the subnormals)."""
+    from parity_util import ParityRun
+    dev = torch.device("cuda", 0)
+    e = np.arange(255, dtype=np.uint16)[:, None]              # biased exponent: one row each
+    c = np.arange(256, dtype=np.uint16)[None, :]              # sign and mantissa: one column each
+    pat = ((c >> 7) << 15) | (e << 7) | (c & 0x7F)            # (255, 256) bf16 bit patterns
+    shapes = [("ex", W.EXPERT, (255, 256)), ("bb", W.BACKBONE, (255, 256)), ("bb.vec", W.BACKBONE, (255 * 256,)),
+              ("rt", W.ROUTER, (255, 256))]
+    specs = [W.Spec(n, tier, shape, k) for k, (n, tier, shape) in enumerate(shapes)]
+    wl = W.Workload("every_bf16", specs, 3)
+    weights = [torch.from_numpy(pat.reshape(shape).astype(np.int16)).view(torch.bfloat16).to(dev).contiguous()
+               for _, _, shape in shapes]
+    log(f"[parity] every finite bf16 weight value, flags {flags}, decay {decay}, 3 steps, all compared")
+    pr = ParityRun(wl, weights=weights, flags=flags, hp=dict(oracle.DEFAULTS, weight_decay=decay))
+    for t in (1, 2, 3):
+        pr.step(t)
+    assert pr.stats.ok(), pr.stats
+
+
 def test_fp32_masters_router_and_norms():
     """Float32 master weights for the router and the vectors (the paper's fp32 router and
     norms, Table 5): updated in float32 with no cast, bit for bit with the oracle, beside

@@ -260,6 +260,35 @@ def test_weights_of_every_finite_bf16_value(flags, decay):
     assert pr.stats.ok(), pr.stats
 
 
+def test_gradients_spanning_the_bf16_exponent_range():
+    """Gradients that take every bf16 value of biased exponent 0 to 140 (zero, the subnormals,
+    both signs, every mantissa; |g| < 2^14, so no sum of squares overflows a float), one
+    exponent per row, in a factored expert matrix, a factored backbone matrix with momentum,
+    an exact-V vector and an exact-V router matrix, rows shuffled differently at each of 3
+    steps; every element against the oracle. Rows of subnormal gradients have R_i = 0 in
+    float beside nonzero elements; every other row spans the eps floor."""
+    from parity_util import ParityRun
+    e = np.arange(141, dtype=np.uint16)[:, None]
+    c = np.arange(256, dtype=np.uint16)[None, :]
+    pat = ((c >> 7) << 15) | (e << 7) | (c & 0x7F)            # (141, 256) bf16 bit patterns
+    shapes = [("ex", W.EXPERT, (141, 256)), ("bb", W.BACKBONE, (141, 256)), ("bb.vec", W.BACKBONE, (141 * 256,)),
+              ("rt", W.ROUTER, (141, 256))]
+    specs = [W.Spec(n, tier, shape, k) for k, (n, tier, shape) in enumerate(shapes)]
+    wl = W.Workload("bf16_range_grads", specs, 3)
+
+    def spread(t, G):
+        rng = np.random.default_rng(1000 + t)
+        for k, (_, _, shape) in enumerate(shapes):
+            g = pat[rng.permutation(141)].reshape(shape)
+            G[k].copy_(torch.from_numpy(g.astype(np.int16)).view(torch.bfloat16).to(G[k].device))
+
+    log("[parity] gradients over bf16 exponents 0..140, 3 steps, all compared")
+    pr = ParityRun(wl)
+    for t in (1, 2, 3):
+        pr.step(t, mutate=spread)
+    assert pr.stats.ok(), pr.stats
+
+
 def test_fp32_masters_router_and_norms():
     """Float32 master weights for the router and the vectors (the paper's fp32 router and
     norms, Table 5): updated in float32 with no cast, bit for bit with the oracle, beside

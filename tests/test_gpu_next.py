@@ -260,19 +260,22 @@ def test_weights_of_every_finite_bf16_value(flags, decay):
     assert pr.stats.ok(), pr.stats
 
 
-def test_gradients_spanning_the_bf16_exponent_range():
+@pytest.mark.parametrize("width", [256, 2048, 8192])
+def test_gradients_spanning_the_bf16_exponent_range(width):
     """Gradients that take every bf16 value of biased exponent 0 to 140 (zero, the subnormals,
     both signs, every mantissa; |g| < 2^14, so no sum of squares overflows a float), one
-    exponent per row, in a factored expert matrix, a factored backbone matrix with momentum,
-    an exact-V vector and an exact-V router matrix, rows shuffled differently at each of 3
-    steps; every element against the oracle. Rows of subnormal gradients have R_i = 0 in
-    float beside nonzero elements; every other row spans the eps floor."""
+    exponent per row (the 256 sign-and-mantissa patterns repeated along rows of `width`), in a
+    factored expert matrix, a factored backbone matrix with momentum, an exact-V vector and
+    an exact-V router matrix, rows shuffled differently at each of 3 steps; every element
+    against the oracle. Rows of subnormal gradients have R_i = 0 in float beside nonzero
+    elements; every other row spans the eps floor. The widths take the row-band pass with one
+    wave per row, two, and eight."""
     from parity_util import ParityRun
     e = np.arange(141, dtype=np.uint16)[:, None]
-    c = np.arange(256, dtype=np.uint16)[None, :]
-    pat = ((c >> 7) << 15) | (e << 7) | (c & 0x7F)            # (141, 256) bf16 bit patterns
-    shapes = [("ex", W.EXPERT, (141, 256)), ("bb", W.BACKBONE, (141, 256)), ("bb.vec", W.BACKBONE, (141 * 256,)),
-              ("rt", W.ROUTER, (141, 256))]
+    c = np.arange(width, dtype=np.uint16)[None, :] & 0xFF
+    pat = ((c >> 7) << 15) | (e << 7) | (c & 0x7F)            # (141, width) bf16 bit patterns
+    shapes = [("ex", W.EXPERT, (141, width)), ("bb", W.BACKBONE, (141, width)), ("bb.vec", W.BACKBONE, (141 * width,)),
+              ("rt", W.ROUTER, (141, width))]
     specs = [W.Spec(n, tier, shape, k) for k, (n, tier, shape) in enumerate(shapes)]
     wl = W.Workload("bf16_range_grads", specs, 3)
 

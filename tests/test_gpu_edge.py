@@ -297,3 +297,24 @@ def test_two_contexts_on_two_streams_match_serial_runs():
         assert oc.clip_info() == osr.clip_info()
         oc.close()
         osr.close()
+
+
+@pytest.mark.parametrize("hp", [
+    dict(beta1=0.0, beta2=0.0),
+    dict(beta1=0.5, beta2=0.5),
+    dict(beta1=0.99, beta2=0.9999, lr=1e-2),
+    dict(eps=1e-30),
+    dict(eps=1e-3),
+    dict(clip_threshold=float("inf")),
+    dict(clip_threshold=1e-3, lr=0.0),
+], ids=["no_memory", "short_memory", "long_memory_high_lr", "floor_1e-30", "floor_1e-3", "no_clipping",
+        "clip_everywhere_lr0"])
+def test_hyper_parameter_extremes_tiny_every_tensor(hp):
+    """The tiny one-layer set (21 tensors in every tier) under hyper-parameters at the edges
+    the step allows: EMAs with no memory (beta = 0: R, C, M and V are this step's), short and
+    very long memories, an eps floor far below or above the second moments, no clipping
+    (threshold +inf), and clipping everywhere with lr = 0 (only the dither acts, and it never
+    moves a weight by itself); 4 steps, every tensor against the oracle."""
+    log(f"[parity] tiny, hyper-parameters {hp}, 4 steps, all compared")
+    st = run(W.get("tiny"), steps=4, hp=dict(oracle.DEFAULTS, **hp))
+    assert st.ok(), st

@@ -557,7 +557,7 @@ __device__ __forceinline__ double rsq_d(double x) {
   return y * fma(-0.5 * x * y, y, 1.5);
 }
 
-template <int NSEG, int RB, bool MOM, bool VEC, bool GN, bool REG_SUMS = false>
+template <int NSEG, int RB, bool MOM, bool VEC, bool GN, int FIXED = 0>
 __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const StepConsts &k, int mode,
                                          unsigned char *bufA, unsigned char *bufB, float *rbA, float *rbB,
                                          double *rowsh, double *sh, float *rstash) {
@@ -569,7 +569,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   // straight into registers by buffer loads while it sums the current one. Lanes past the row's end and rows past the
   // band's end take an offset beyond the buffer's range, so the hardware returns zeros for
   // them. The planner keeps a block's byte span below 2^31 for these tensors.
-  constexpr bool REG = VEC && !MOM && NSEG <= 2 && (!GN || REG_SUMS);
+  constexpr bool REG = VEC && !MOM && NSEG <= 2 && (!GN || FIXED != 0);
   const int wpr = (zcw + NSEG - 1) / NSEG;   // waves per row
   const int grp = wave / wpr;
   const int wg = wave - grp * wpr;           // wave within the group
@@ -847,7 +847,7 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
       const int b = lane / P, w = lane - b * P;
       const int r = grp_c * rb + (b < rb ? b : 0);
       const int64_t i = rbase + r;
-      const float R = rcur[r];
+      const float R = REG ? rold : rcur[r];   // (REG: the folded R of the lane's row r)
       const double Rd = (double)R;
       const bool normal = R > 0.f && R < __builtin_inff();
       winv_l = (normal && i < r1) ? rcp_d(Rd) : 0.0;   // (1/R is 0 for R = +inf)
@@ -1063,8 +1063,9 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
 
 // GN: the gradient-norm mode's passes (mode 1, the sums of g^2 alone, or mode 2, z and the
 // floored sum of the scaled gradient once R is folded); without it the mode is 0 at compile
-// time. RS: the sums pass with the mode fixed to 1 at compile time, staged in registers.
-template <int NSEG, bool MOM, bool VEC, bool GN, bool RS = false>
+// time. FIXED: one of those passes (1 or 2) with its mode fixed at compile time, staged in
+// registers.
+template <int NSEG, bool MOM, bool VEC, bool GN, int FIXED = 0>
 __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restrict__ TT,
                                                         const Item *__restrict__ items, StepConsts k, int mode_arg) {
   __shared__ __attribute__((aligned(16))) unsigned char bufA[kZLdsBytes + 2048];
@@ -1077,17 +1078,19 @@ __global__ __launch_bounds__(kZThreads) void p1z_kernel(const DevTensor *__restr
   reinterpret_cast<uint32_t *>(bufA + kZLdsBytes)[threadIdx.x] = 0u;
   reinterpret_cast<uint32_t *>(bufB + kZLdsBytes)[threadIdx.x] = 0u;
   static_assert(kZThreads * 4 == 2048, "one word per thread");
-  const int mode = RS ? 1 : GN ? mode_arg : 0;
+  const int mode = FIXED != 0 ? FIXED : GN ? mode_arg : 0;
   const Item it = items[blockIdx.x];
   const DevTensor &t = TT[it.tensor];
   // rows per group and block: the planner keeps 4 at most with one or two chunks per wave,
   // 2 with three and 1 with four, which keeps every variant's loop free of register spills
+  // (the gradient-norm mode's register-staged z pass takes 2: with 4 its registers spill)
+  constexpr int RB4 = FIXED == 2 ? 2 : 4;
   if (NSEG <= 2 && t.zrb >= 4)
-    p1z_body<NSEG, NSEG <= 2 ? 4 : 1, MOM, VEC, GN, RS>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG <= 2 ? RB4 : 1, MOM, VEC, GN, FIXED>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else if (NSEG <= 3 && t.zrb >= 2)
-    p1z_body<NSEG, NSEG <= 3 ? 2 : 1, MOM, VEC, GN, RS>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, NSEG <= 3 ? 2 : 1, MOM, VEC, GN, FIXED>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
   else
-    p1z_body<NSEG, 1, MOM, VEC, GN, RS>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
+    p1z_body<NSEG, 1, MOM, VEC, GN, FIXED>(t, it.tile, k, mode, bufA, bufB, rbA, rbB, rowsh, sh, rstash);
 }
 
 // Reductions of the clip stage, over the whole work-group (a tensor of its own) or over one
@@ -2279,8 +2282,11 @@ int launch_p1z(const DevTensor *T, const Item *items, int64_t count, const StepC
 #define SKEW_P1Z_CASE(V, NSEG, VEC, MOM)                                                          \
   case V:                                                                                          \
     if (mode == 1)                                                                                 \
-      hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, true, (NSEG <= 2 && VEC && !MOM)>), grid, block, \
-                         0, s, T, items, k, 1);                                                   \
+      hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, true, (NSEG <= 2 && VEC && !MOM) ? 1 : 0>), grid, \
+                         block, 0, s, T, items, k, 1);                                            \
+    else if (mode == 2)                                                                            \
+      hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, true, (NSEG <= 2 && VEC && !MOM) ? 2 : 0>), grid, \
+                         block, 0, s, T, items, k, 2);                                            \
     else if (mode != 0)                                                                            \
       hipLaunchKernelGGL((p1z_kernel<NSEG, MOM, VEC, true>), grid, block, 0, s, T, items, k, mode); \
     else                                                                                           \

@@ -399,7 +399,7 @@ __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restric
 //
 // Staging: blocks of zrpi * zrb whole rows (bf16 gradient, and fp32 momentum on the
 // backbone). Aligned rows without momentum and with one or two chunks per wave (the normal
-// step, and the gradient-norm mode's sums pass) stage in registers: each wave loads its own
+// step, and the gradient-norm mode's two passes) stage in registers: each wave loads its own
 // pieces of the next block by buffer loads while it sums the current one. The other variants move a block into one of two LDS
 // buffers while the other is being summed: with the direct global-to-LDS loads (16 bytes
 // per lane) when rows are 16-byte aligned, through registers otherwise; no register holds
@@ -564,11 +564,12 @@ __device__ __forceinline__ void p1z_body(const DevTensor &t, int band, const Ste
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t m = t.m, ld = t.ld;
   const int zcw = t.zcw;
-  // Register staging (aligned rows, no momentum, up to two chunks per wave, the normal step
-  // or the gradient-norm mode's sums pass): each wave loads its own pieces of the next block
-  // straight into registers by buffer loads while it sums the current one. Lanes past the row's end and rows past the
-  // band's end take an offset beyond the buffer's range, so the hardware returns zeros for
-  // them. The planner keeps a block's byte span below 2^31 for these tensors.
+  // Register staging (aligned rows, no momentum, up to two chunks per wave; the normal step
+  // or a gradient-norm pass with its mode fixed at compile time): each wave loads its own
+  // pieces of the next block straight into registers by buffer loads while it sums the
+  // current one. Lanes past the row's end and rows past the band's end take an offset beyond
+  // the buffer's range, so the hardware returns zeros for them. The planner keeps a block's
+  // byte span below 2^31 for these tensors.
   constexpr bool REG = VEC && !MOM && NSEG <= 2 && (!GN || FIXED != 0);
   const int wpr = (zcw + NSEG - 1) / NSEG;   // waves per row
   const int grp = wave / wpr;

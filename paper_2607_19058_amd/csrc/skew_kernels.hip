@@ -400,11 +400,11 @@ __global__ __launch_bounds__(kThreads) void p1_kernel(const DevTensor *__restric
 // Staging: blocks of zrpi * zrb whole rows (bf16 gradient, and fp32 momentum on the
 // backbone). Aligned rows without momentum and with one or two chunks per wave (the normal
 // step, and the gradient-norm mode's two passes) stage in registers: each wave loads its own
-// pieces of the next block by buffer loads while it sums the current one. The other variants move a block into one of two LDS
-// buffers while the other is being summed: with the direct global-to-LDS loads (16 bytes
-// per lane) when rows are 16-byte aligned, through registers otherwise; no register holds
-// their data in flight, so a 512-thread work-group with up to 256 VGPRs per wave keeps a
-// whole block (up to 64 KiB) of loads outstanding.
+// pieces of the next block by buffer loads while it sums the current one. The other variants
+// move a block into one of two LDS buffers while the other is being summed: with the direct
+// global-to-LDS loads (16 bytes per lane) when rows are 16-byte aligned, through registers
+// otherwise; no register holds their data in flight, so a 512-thread work-group with up to
+// 256 VGPRs per wave keeps a whole block (up to 64 KiB) of loads outstanding.
 //
 // Layout: zcw 512-column chunks per row; a group of wpr = ceil(zcw / NSEG) waves shares a
 // row, wave w of the group taking chunks w, w + wpr, ...; zrpi = 8 / wpr groups work on

@@ -34,6 +34,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -85,8 +86,20 @@ def algorithmic_bytes(specs) -> int:
     return total
 
 
+# comments and C string/char literals of the kernel source, in source order
+_C_TOKENS = re.compile(r'//[^\n]*|/\*.*?\*/|"(?:\\.|[^"\\\n])*"|\'(?:\\.|[^\'\\\n])*\'', re.S)
+
+
+def code_hash(src: str) -> str:
+    """sha256[:16] of C/C++ source with its comments removed and whitespace collapsed."""
+    code = _C_TOKENS.sub(lambda mt: " " if mt.group(0)[0] == "/" else mt.group(0), src)
+    return hashlib.sha256(" ".join(code.split()).encode()).hexdigest()[:16]
+
+
 def kernel_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """The kernel source's code hash: the stored counters stay tied to the code they were
+    taken on, not to its comments."""
+    return code_hash(open(KERNEL_SRC, encoding="utf-8").read())
 
 
 def cpu_model() -> str:

@@ -248,6 +248,9 @@ def main() -> int:
                     help="steps of the separate pass that times each kernel with HIP events")
     ap.add_argument("--no-ceilings", action="store_true", help="skip the in-process copy/read ceilings")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0 or args.kernel_steps < 1:
+        ap.error("--steps and --kernel-steps must be at least 1 and --warmup at least 0 (the roofline's "
+                 "per-kernel times come from the --kernel-steps pass)")
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} (WORLD_SIZE {world}) is not supported: "

@@ -31,3 +31,13 @@ def test_stored_counters_match_the_kernel_code():
     for name in ("traffic_full.json", "traffic_full_tiers.json"):
         tr = json.load(open(os.path.join(ROOT, "profiles", name)))
         assert tr["kernel_src_sha"] == bench.kernel_sha(), name
+
+
+def test_bench_refuses_step_counts_it_cannot_time():
+    """No per-kernel timing pass (or no timed step) would leave the roofline without a
+    duration: the arguments are refused before any device work."""
+    import subprocess
+    for bad in (["--kernel-steps", "0"], ["--steps", "0"], ["--warmup", "-1"]):
+        r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py")] + bad, capture_output=True, text=True,
+                           timeout=120)
+        assert r.returncode == 2 and "at least" in r.stderr, (bad, r.stderr[-300:])
